@@ -1,0 +1,233 @@
+#!/usr/bin/env python3
+"""W4A4 linear benchmark on one MI355X: effective TOPS on the FLUX-12B MLP linears.
+
+One step = the whole hot path (per-token int4 quantisation of the activations,
+packed int4 GEMM with int32 accumulation, fused dequantising epilogue) for both
+FLUX-12B MLP linears back-to-back:
+  up:   X [4608, 3072] -> N = 12288, with bias
+  down: X [9216, 12288] -> N = 3072 (two images)
+Weights are packed once before timing (offline, as at model load).  Inputs are
+seeded synthetic tensors already resident in HBM.
+
+value = sum(2 M N K) / step time, in TOPS.  The line also carries the roofline
+of the dominant kernel (the down-projection GEMM), timed per launch with HIP
+events on the stream the library launches on, and the CPU oracle timed on a
+bounded sample of the same rows on the host cores.
+"""
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_INT8_TOPS = 5000.0     # MI355X dense int8 MFMA, published
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E, published
+
+
+def parse_args():
+    p = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=200)
+    p.add_argument("--warmup", type=int, default=20)
+    p.add_argument("--no-cpu-baseline", action="store_true", help="skip the oracle CPU baseline leg")
+    p.add_argument("--cpu-seconds", type=float, default=12.0, help="target CPU time of the oracle sample")
+    return p.parse_args()
+
+
+def log(*a):
+    print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+class Prepared:
+    """Device-resident inputs, packed weight and output/workspace buffers of one linear."""
+
+    def __init__(self, lin, torch, jq):
+        self.lin = lin
+        self.x_bits = lin.make_x()
+        self.w_bits = lin.make_w()
+        self.b_bits = lin.make_bias()
+        self.x = jq.bf16_tensor(self.x_bits, "cuda")
+        w = jq.bf16_tensor(self.w_bits, "cuda")
+        self.wq, self.sw = jq.jq_pack_weight_int4(w)
+        del w
+        self.b = None if self.b_bits is None else jq.bf16_tensor(self.b_bits, "cuda")
+        self.y = torch.empty((lin.M, lin.N), dtype=torch.bfloat16, device="cuda")
+        self.ws = torch.empty(jq.jq_w4a4_workspace_bytes(lin.M, lin.K), dtype=torch.uint8, device="cuda")
+        self.q = torch.empty((lin.M, lin.K // 2), dtype=torch.uint8, device="cuda")
+        self.s = torch.empty((lin.M,), dtype=torch.float32, device="cuda")
+
+
+def cpu_baseline(preps, target_s):
+    """The oracle as it stands, on a bounded sample of rows of each linear."""
+    import numpy as np
+    import oracle
+    from paper_2609_33601_amd import jq
+
+    try:
+        from threadpoolctl import threadpool_info
+
+        blas = [i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"]
+        cores = max(blas) if blas else 1
+    except Exception:  # noqa: BLE001
+        cores = 1
+    packed = [oracle.pack_weight_int4(p.w_bits) for p in preps]  # offline step, untimed
+
+    def run(nrows):
+        ops = 0
+        outs = []
+        t0 = time.perf_counter()
+        for p, (rq, rs) in zip(preps, packed):
+            rows = np.linspace(0, p.lin.M - 1, nrows).astype(np.int64)
+            outs.append((rows, oracle.w4a4_linear_rows(p.x_bits, rq, rs, rows, p.b_bits)))
+            ops += 2 * nrows * p.lin.N * p.lin.K
+        return time.perf_counter() - t0, ops, outs
+
+    t, _, _ = run(8)
+    nrows = int(max(8, min(min(p.lin.M for p in preps), 8 * target_s / max(t, 1e-6))))
+    t, ops, outs = run(nrows)
+    # the sample doubles as a parity check of the GPU outputs on the same rows
+    mism = 0
+    for p, (rows, ref) in zip(preps, outs):
+        got = jq.bf16_bits(p.y[torch_index(rows)])
+        mism += int(np.sum(got != ref))
+    return {
+        "value": ops / t / 1e12,
+        "unit": "TOPS",
+        "cores": int(cores),
+        "kind": "oracle",
+        "sample": f"{nrows} evenly spaced rows of each of the {len(preps)} linears "
+                  f"({ops / 1e9:.1f} G int ops, {t:.1f} s; weights packed beforehand)",
+        "seconds": t,
+        "host_cpus": os.cpu_count(),
+        "affinity_cpus": len(os.sched_getaffinity(0)),
+        "gpu_rows_differing_from_oracle": mism,
+    }
+
+
+def torch_index(rows):
+    import torch
+
+    return torch.from_numpy(rows).cuda()
+
+
+def main():
+    args = parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the W4A4 linear "
+              "shards without communication over tokens (M) and is measured at N=1.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2609_33601_amd import jq, workloads
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    jq.lib()
+    wl = workloads.FLUX_MLP
+    log("preparing", wl.description)
+    preps = [Prepared(lin, torch, jq) for lin in wl.linears]
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+
+    def step():
+        for p in preps:
+            jq.jq_w4a4_linear(p.x, p.wq, p.sw, p.b, y=p.y, workspace=p.ws)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev0.record(stream)
+    for _ in range(args.steps):
+        step()
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_per_step = ev0.elapsed_time(ev1) / args.steps
+    value = wl.ops / (ms_per_step * 1e-3) / 1e12
+    log(f"timed {args.steps} steps: {ms_per_step * 1e3:.1f} us/step (wall {wall * 1e3 / args.steps:.1f} us/step)")
+
+    # Per-kernel durations: the same two kernels the linear launches, bracketed by events.
+    n_launch = max(args.steps, 20)
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(len(preps) * n_launch)]
+    for it in range(n_launch):
+        for j, p in enumerate(preps):
+            e = evs[it * len(preps) + j]
+            e[0].record(stream)
+            jq.jq_quantize_act(p.x, q=p.q, scale=p.s)
+            e[1].record(stream)
+            jq.jq_w4a4_gemm(p.q, p.s, p.wq, p.sw, p.b, y=p.y)
+            e[2].record(stream)
+    torch.cuda.synchronize()
+    kernels = []
+    for j, p in enumerate(preps):
+        lin = p.lin
+        tq = sum(evs[it * len(preps) + j][0].elapsed_time(evs[it * len(preps) + j][1]) for it in range(n_launch))
+        tg = sum(evs[it * len(preps) + j][1].elapsed_time(evs[it * len(preps) + j][2]) for it in range(n_launch))
+        tq_us, tg_us = tq / n_launch * 1e3, tg / n_launch * 1e3
+        q_bytes = 2 * lin.M * lin.K + lin.M * lin.K // 2 + 4 * lin.M
+        g_ops = 2 * lin.M * lin.N * lin.K
+        kernels.append({"linear": lin.name, "kernel": "quantize_rows", "avg_us": tq_us,
+                        "algorithmic_bytes": q_bytes, "achieved_GBs": q_bytes / tq_us / 1e3,
+                        "frac_hbm_peak": q_bytes / tq_us / 1e3 / PEAK_HBM_GBS})
+        kernels.append({"linear": lin.name, "kernel": "w4a4_gemm", "avg_us": tg_us, "ops": g_ops,
+                        "achieved_TOPS": g_ops / tg_us / 1e6,
+                        "frac_int8_peak": g_ops / tg_us / 1e6 / PEAK_INT8_TOPS})
+        log(f"{lin.name}: quantize {tq_us:.1f} us ({q_bytes / tq_us / 1e3:.0f} GB/s), "
+            f"gemm {tg_us:.1f} us ({g_ops / tg_us / 1e6:.0f} TOPS)")
+    dom = max((k for k in kernels if k["kernel"] == "w4a4_gemm"), key=lambda k: k["ops"])
+    roofline = {"bound": "mfma", "achieved": dom["achieved_TOPS"], "peak": PEAK_INT8_TOPS, "unit": "TOP/s",
+                "frac": dom["achieved_TOPS"] / PEAK_INT8_TOPS, "traffic": None,
+                "kernel": f"w4a4_gemm ({dom['linear']})", "avg_launch_us": dom["avg_us"]}
+
+    # Re-run the timed configuration once so that y holds the linear's outputs for the parity sample.
+    step()
+    torch.cuda.synchronize()
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(preps, args.cpu_seconds)
+        log(f"cpu oracle: {cpu['value']:.4f} TOPS on {cpu['cores']} threads; {cpu['sample']}; "
+            f"gpu/oracle differing outputs on the sample: {cpu['gpu_rows_differing_from_oracle']}")
+
+    props = torch.cuda.get_device_properties(0)
+    out = {
+        "metric": "W4A4 linear effective TOPS + % int8 MFMA peak at FLUX-12B MLP shape",
+        "value": value,
+        "unit": "TOPS",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int8",
+        "data": "synthetic (seeded; FLUX-12B MLP activation/weight statistics)",
+        "pct_int8_peak": 100.0 * value / PEAK_INT8_TOPS,
+        "config": {
+            "workload": wl.description,
+            "linears": [{"name": l.name, "M": l.M, "K": l.K, "N": l.N, "bias": l.bias_std is not None}
+                        for l in wl.linears],
+            "ops_per_step": wl.ops,
+            "parallelism": "none (1 GPU)",
+            "device": f"{props.name} {getattr(props, 'gcnArchName', '')} CUs={props.multi_processor_count}",
+        },
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+        "kernels": kernels,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,152 @@
+/*
+ * jq.h -- C ABI of libjq, an MI355X (gfx950) implementation of the plain W4A4
+ * linear layer: dynamic per-token symmetric int4 activation quantisation, an
+ * int4 x int4 matrix product with exact int32 accumulation and a dequantising
+ * epilogue that writes bf16.
+ *
+ * The operator.  The paper's quantised network keeps the topology of the
+ * full-precision one and replaces each module by a low-bit operator of the
+ * deployment family (Sec. 3.1 "Quantization as distillation"); for W4A4 that
+ * family is INT4 weights and INT4 activations (appendix "Experimental
+ * Details", quantization-function rows), executed by quantisation, packing and
+ * low-bit matrix-multiplication kernels with no smoothing, rotation,
+ * normalisation or SVD branch (appendix FAQ Q7).  The paper states no formula,
+ * so the library implements this reading of it, per row r of a bf16 matrix:
+ *
+ *     a_r    = max_k |x[r,k]|
+ *     s_r    = fl32(a_r / 7)                                  (IEEE fp32 division)
+ *     q[r,k] = clamp(rne(fl32(x[r,k] / s_r)), -8, 7),  q = 0 if s_r = 0
+ *
+ * (rne = round half to even).  Activations X[M,K] get one scale per token
+ * (row), weights W[N,K] one scale per output channel (row).  The layer is
+ *
+ *     acc[m,n] = sum_k qx[m,k] * qw[n,k]                       (exact integer)
+ *     y[m,n]   = bf16_rne(((fl32(acc) * s_x[m]) * s_w[n]) + bias[n])
+ *
+ * with each fp32 operation rounded on its own (no fused multiply-add).
+ *
+ * Packed int4 layout (activations and weights alike): row-major [rows, K/2]
+ * bytes; byte j of a row holds code 2j in its low nibble and code 2j+1 in its
+ * high nibble, both as 4-bit two's complement.
+ *
+ * Conventions for every call:
+ *   - All tensor pointers are DEVICE pointers, owned by the caller; the library
+ *     never allocates device memory, never synchronises and never prints.
+ *   - Every call is asynchronous on `stream` (a hipStream_t passed as void*;
+ *     NULL means the default stream).  Outputs are valid once the stream has
+ *     reached the call.
+ *   - Matrices are contiguous and row-major.  bf16 is passed as raw 16-bit
+ *     patterns (void*).
+ *   - Shapes: rows (M, N) >= 1; K >= 64 and K % 64 == 0, else
+ *     JQ_ERR_UNSUPPORTED_SHAPE; K <= 65536 so that every accumulator stays
+ *     exact in int32 and in fp32; rows <= 2^30 and, for the GEMM calls,
+ *     ceil(M/256) * ceil(N/256) <= 2^26, else JQ_ERR_UNSUPPORTED_SHAPE.
+ *     Non-positive sizes or required NULL pointers give JQ_ERR_INVALID_ARG.
+ *   - Matrix and packed pointers must be 16-byte aligned and scale/bias pointers
+ *     4-/2-byte aligned, else JQ_ERR_MISALIGNED.
+ *   - Arguments are checked before anything is launched: on any error nothing
+ *     is written.  A failed kernel launch returns JQ_ERR_HIP; faults during
+ *     execution surface at the caller's next synchronisation.
+ *   - There is no global mutable state: calls may be made from several host
+ *     threads at once (on one stream they execute in issue order).
+ */
+#ifndef JQ_H
+#define JQ_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  JQ_OK = 0,
+  JQ_ERR_INVALID_ARG = 1,
+  JQ_ERR_UNSUPPORTED_SHAPE = 2,
+  JQ_ERR_MISALIGNED = 3,
+  JQ_ERR_WORKSPACE_TOO_SMALL = 4,
+  JQ_ERR_HIP = 5
+} jq_status;
+
+/* Human-readable name of a status code (static string, never NULL). */
+const char* jq_status_string(jq_status s);
+
+/* Library version as major*10000 + minor*100 + patch. */
+int jq_version(void);
+
+/*
+ * Activation quantisation (Sec. 3.1; FAQ Q7: the quantisation and packing
+ * kernel).  Quantises each row (token) of x_bf16 [M,K] with its own scale.
+ *   x_bf16   in   [M,K] bf16, 16-byte aligned
+ *   q_packed out  [M,K/2] uint8 in the packed layout above, 16-byte aligned
+ *   scale    out  [M] fp32, s_r as defined above
+ * Errors: JQ_ERR_INVALID_ARG, JQ_ERR_UNSUPPORTED_SHAPE, JQ_ERR_MISALIGNED, JQ_ERR_HIP.
+ */
+jq_status jq_quantize_act(const void* x_bf16, int64_t M, int64_t K,
+                          void* q_packed, float* scale, void* stream);
+
+/*
+ * Weight quantisation and packing (Sec. 3.1; FAQ Q7), done once per layer
+ * when a model is loaded.  Per-output-channel scaling of W [N,K] is the same
+ * row quantiser applied to the rows of W.
+ *   w_bf16    in   [N,K] bf16
+ *   wq_packed out  [N,K/2] uint8 (packed layout above)
+ *   w_scale   out  [N] fp32
+ * Errors: as jq_quantize_act.
+ */
+jq_status jq_pack_weight_int4(const void* w_bf16, int64_t N, int64_t K,
+                              void* wq_packed, float* w_scale, void* stream);
+
+/*
+ * Bytes of device workspace jq_w4a4_linear needs for an [M,K] input: the
+ * packed activations (M*K/2 bytes) and their scales (4*M bytes), each part
+ * rounded up to 256 bytes.  Returns 0 for invalid sizes.
+ */
+size_t jq_w4a4_workspace_bytes(int64_t M, int64_t K);
+
+/*
+ * The whole W4A4 linear (Sec. 3.1, FAQ Q7): quantise x per token into the
+ * workspace, then the int4 GEMM with the fused epilogue.
+ *   x_bf16      in   [M,K] bf16
+ *   wq_packed   in   [N,K/2] uint8 from jq_pack_weight_int4
+ *   w_scale     in   [N] fp32 from jq_pack_weight_int4
+ *   bias_bf16   in   [N] bf16, or NULL for no bias
+ *   y_bf16      out  [M,N] bf16, 16-byte aligned
+ *   workspace   scratch of at least jq_w4a4_workspace_bytes(M,K) bytes,
+ *               256-byte aligned, owned by the caller; its contents on return
+ *               are the packed activations followed by their scales.
+ * Errors: as jq_quantize_act, plus JQ_ERR_WORKSPACE_TOO_SMALL.
+ */
+jq_status jq_w4a4_linear(const void* x_bf16, int64_t M, int64_t K,
+                         const void* wq_packed, const float* w_scale, int64_t N,
+                         const void* bias_bf16, void* y_bf16,
+                         void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * GEMM + epilogue on already-quantised activations (Sec. 3.1, FAQ Q7: the
+ * low-bit matrix multiplication).  Lets several linears that read the same
+ * input share one quantisation.
+ *   q_packed, scale   in  [M,K/2] uint8 and [M] fp32 from jq_quantize_act
+ *   wq_packed, w_scale, bias_bf16, y_bf16: as jq_w4a4_linear
+ * Errors: JQ_ERR_INVALID_ARG, JQ_ERR_UNSUPPORTED_SHAPE, JQ_ERR_MISALIGNED, JQ_ERR_HIP.
+ */
+jq_status jq_w4a4_gemm(const void* q_packed, const float* scale, int64_t M, int64_t K,
+                       const void* wq_packed, const float* w_scale, int64_t N,
+                       const void* bias_bf16, void* y_bf16, void* stream);
+
+/*
+ * The exact integer contraction alone, for checking (Sec. 3.1, FAQ Q7):
+ * acc[m,n] = sum_k qx[m,k] * qw[n,k] written as int32 [M,N] (16-byte aligned),
+ * computed by the same kernel as jq_w4a4_gemm with the epilogue replaced by a
+ * plain store.
+ * Errors: JQ_ERR_INVALID_ARG, JQ_ERR_UNSUPPORTED_SHAPE, JQ_ERR_MISALIGNED, JQ_ERR_HIP.
+ */
+jq_status jq_w4a4_gemm_i32(const void* q_packed, int64_t M, int64_t K,
+                           const void* wq_packed, int64_t N, int32_t* acc, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* JQ_H */

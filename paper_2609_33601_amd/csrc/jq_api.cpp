@@ -1,0 +1,127 @@
+// C ABI of libjq: argument checks, workspace layout and kernel launches.
+// Every check runs before any launch, so a rejected call writes nothing.
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "jq.h"
+#include "jq_internal.h"
+
+namespace {
+
+constexpr size_t kWsAlign = 256;
+
+size_t round_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+// Shape checks shared by every entry point: rows >= 1, 64 <= K <= kMaxK, K % 64 == 0.
+jq_status check_shape(int64_t rows, int64_t K) {
+  if (rows <= 0 || K <= 0) return JQ_ERR_INVALID_ARG;
+  if (rows > jq::kMaxRows) return JQ_ERR_UNSUPPORTED_SHAPE;
+  if (K < 64 || K % 64 != 0 || K > jq::kMaxK) return JQ_ERR_UNSUPPORTED_SHAPE;
+  return JQ_OK;
+}
+
+jq_status from_hip(hipError_t e) { return e == hipSuccess ? JQ_OK : JQ_ERR_HIP; }
+
+hipStream_t as_stream(void* s) { return static_cast<hipStream_t>(s); }
+
+jq_status quantize_common(const void* x, int64_t rows, int64_t K, void* q, float* scale, void* stream) {
+  if (x == nullptr || q == nullptr || scale == nullptr) return JQ_ERR_INVALID_ARG;
+  const jq_status st = check_shape(rows, K);
+  if (st != JQ_OK) return st;
+  if (!aligned(x, 16) || !aligned(q, 16) || !aligned(scale, 4)) return JQ_ERR_MISALIGNED;
+  return from_hip(jq::launch_quantize_rows(static_cast<const uint16_t*>(x), rows, K,
+                                           static_cast<uint8_t*>(q), scale, as_stream(stream)));
+}
+
+jq_status check_gemm(const void* qx, const float* sx, int64_t M, int64_t K, const void* qw,
+                     const float* sw, int64_t N, const void* bias, const void* y, bool need_scales) {
+  if (qx == nullptr || qw == nullptr || y == nullptr) return JQ_ERR_INVALID_ARG;
+  if (need_scales && (sx == nullptr || sw == nullptr)) return JQ_ERR_INVALID_ARG;
+  jq_status st = check_shape(M, K);
+  if (st != JQ_OK) return st;
+  st = check_shape(N, K);
+  if (st != JQ_OK) return st;
+  // The tile grid is indexed with 32-bit integers.
+  if (((M + 255) / 256) * ((N + 255) / 256) > (int64_t(1) << 26)) return JQ_ERR_UNSUPPORTED_SHAPE;
+  if (!aligned(qx, 16) || !aligned(qw, 16) || !aligned(y, 16)) return JQ_ERR_MISALIGNED;
+  if ((sx != nullptr && !aligned(sx, 4)) || (sw != nullptr && !aligned(sw, 4))) return JQ_ERR_MISALIGNED;
+  if (bias != nullptr && !aligned(bias, 2)) return JQ_ERR_MISALIGNED;
+  return JQ_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* jq_status_string(jq_status s) {
+  switch (s) {
+    case JQ_OK: return "JQ_OK";
+    case JQ_ERR_INVALID_ARG: return "JQ_ERR_INVALID_ARG";
+    case JQ_ERR_UNSUPPORTED_SHAPE: return "JQ_ERR_UNSUPPORTED_SHAPE";
+    case JQ_ERR_MISALIGNED: return "JQ_ERR_MISALIGNED";
+    case JQ_ERR_WORKSPACE_TOO_SMALL: return "JQ_ERR_WORKSPACE_TOO_SMALL";
+    case JQ_ERR_HIP: return "JQ_ERR_HIP";
+  }
+  return "JQ_ERR_UNKNOWN";
+}
+
+int jq_version(void) { return 100; }
+
+jq_status jq_quantize_act(const void* x_bf16, int64_t M, int64_t K, void* q_packed, float* scale,
+                          void* stream) {
+  return quantize_common(x_bf16, M, K, q_packed, scale, stream);
+}
+
+jq_status jq_pack_weight_int4(const void* w_bf16, int64_t N, int64_t K, void* wq_packed,
+                              float* w_scale, void* stream) {
+  return quantize_common(w_bf16, N, K, wq_packed, w_scale, stream);
+}
+
+size_t jq_w4a4_workspace_bytes(int64_t M, int64_t K) {
+  if (check_shape(M, K) != JQ_OK) return 0;
+  return round_up(static_cast<size_t>(M) * static_cast<size_t>(K / 2), kWsAlign) +
+         round_up(static_cast<size_t>(M) * sizeof(float), kWsAlign);
+}
+
+jq_status jq_w4a4_linear(const void* x_bf16, int64_t M, int64_t K, const void* wq_packed,
+                         const float* w_scale, int64_t N, const void* bias_bf16, void* y_bf16,
+                         void* workspace, size_t workspace_bytes, void* stream) {
+  if (x_bf16 == nullptr || workspace == nullptr) return JQ_ERR_INVALID_ARG;
+  jq_status st = check_gemm(x_bf16, w_scale, M, K, wq_packed, w_scale, N, bias_bf16, y_bf16, true);
+  if (st != JQ_OK) return st;
+  if (!aligned(workspace, kWsAlign)) return JQ_ERR_MISALIGNED;
+  if (workspace_bytes < jq_w4a4_workspace_bytes(M, K)) return JQ_ERR_WORKSPACE_TOO_SMALL;
+
+  uint8_t* qx = static_cast<uint8_t*>(workspace);
+  float* sx = reinterpret_cast<float*>(qx + round_up(static_cast<size_t>(M) * static_cast<size_t>(K / 2), kWsAlign));
+  hipError_t e = jq::launch_quantize_rows(static_cast<const uint16_t*>(x_bf16), M, K, qx, sx,
+                                          as_stream(stream));
+  if (e != hipSuccess) return JQ_ERR_HIP;
+  e = jq::launch_w4a4_gemm(jq::Epilogue::kBf16, qx, sx, M, K, static_cast<const uint8_t*>(wq_packed),
+                           w_scale, N, static_cast<const uint16_t*>(bias_bf16), y_bf16, as_stream(stream));
+  return from_hip(e);
+}
+
+jq_status jq_w4a4_gemm(const void* q_packed, const float* scale, int64_t M, int64_t K,
+                       const void* wq_packed, const float* w_scale, int64_t N, const void* bias_bf16,
+                       void* y_bf16, void* stream) {
+  const jq_status st = check_gemm(q_packed, scale, M, K, wq_packed, w_scale, N, bias_bf16, y_bf16, true);
+  if (st != JQ_OK) return st;
+  return from_hip(jq::launch_w4a4_gemm(jq::Epilogue::kBf16, static_cast<const uint8_t*>(q_packed), scale,
+                                       M, K, static_cast<const uint8_t*>(wq_packed), w_scale, N,
+                                       static_cast<const uint16_t*>(bias_bf16), y_bf16, as_stream(stream)));
+}
+
+jq_status jq_w4a4_gemm_i32(const void* q_packed, int64_t M, int64_t K, const void* wq_packed, int64_t N,
+                           int32_t* acc, void* stream) {
+  const jq_status st = check_gemm(q_packed, nullptr, M, K, wq_packed, nullptr, N, nullptr, acc, false);
+  if (st != JQ_OK) return st;
+  return from_hip(jq::launch_w4a4_gemm(jq::Epilogue::kInt32, static_cast<const uint8_t*>(q_packed),
+                                       nullptr, M, K, static_cast<const uint8_t*>(wq_packed), nullptr, N,
+                                       nullptr, acc, as_stream(stream)));
+}
+
+}  // extern "C"

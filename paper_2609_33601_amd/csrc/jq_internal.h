@@ -1,0 +1,33 @@
+// Internal launch interface between the C ABI layer and the gfx950 kernels.
+#ifndef JQ_INTERNAL_H
+#define JQ_INTERNAL_H
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace jq {
+
+// Largest supported reduction length.  With codes in [-8, 7] the kernel's
+// int8 operands are 16 * code, so its int32 accumulator holds 256 * acc with
+// |256 * acc| <= 256 * 64 * K = 2^30 at K = 65536, and |acc| < 2^24 keeps the
+// epilogue's int -> fp32 conversion exact.
+constexpr int64_t kMaxK = 65536;
+// Rows are addressed with 32-bit block indices.
+constexpr int64_t kMaxRows = int64_t(1) << 30;
+
+// Row quantiser: x [M,K] bf16 -> q [M,K/2] packed int4, scale [M] fp32.
+hipError_t launch_quantize_rows(const uint16_t* x, int64_t M, int64_t K, uint8_t* q, float* scale,
+                                hipStream_t st);
+
+enum class Epilogue { kBf16, kInt32 };
+
+// Packed int4 GEMM: acc[m,n] = sum_k qx[m,k] * qw[n,k] followed by the epilogue.
+//   kBf16:  y[m,n] = bf16(((fp32(acc) * sx[m]) * sw[n]) + bias[n])  (bias may be null)
+//   kInt32: out[m,n] = acc
+hipError_t launch_w4a4_gemm(Epilogue epi, const uint8_t* qx, const float* sx, int64_t M, int64_t K,
+                            const uint8_t* qw, const float* sw, int64_t N, const uint16_t* bias,
+                            void* out, hipStream_t st);
+
+}  // namespace jq
+
+#endif  // JQ_INTERNAL_H

@@ -1,0 +1,206 @@
+"""Python binding of libjq (include/jq.h): argument marshalling only.
+
+Every function takes torch tensors that live on the GPU, passes their device
+pointers and the current HIP stream to the C ABI, and raises JQError on a
+non-OK status.  All arithmetic happens in the HIP kernels; if libjq.so is not
+built, every call raises instead of computing anything another way.
+"""
+
+import ctypes
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libjq.so")
+
+JQ_OK = 0
+JQ_ERR_INVALID_ARG = 1
+JQ_ERR_UNSUPPORTED_SHAPE = 2
+JQ_ERR_MISALIGNED = 3
+JQ_ERR_WORKSPACE_TOO_SMALL = 4
+JQ_ERR_HIP = 5
+
+# Symbols the library exports, with (restype, argtypes).
+_vp, _i64, _sz, _fp, _ip = ctypes.c_void_p, ctypes.c_int64, ctypes.c_size_t, ctypes.c_void_p, ctypes.c_void_p
+SIGNATURES = {
+    "jq_status_string": (ctypes.c_char_p, [ctypes.c_int]),
+    "jq_version": (ctypes.c_int, []),
+    "jq_quantize_act": (ctypes.c_int, [_vp, _i64, _i64, _vp, _fp, _vp]),
+    "jq_pack_weight_int4": (ctypes.c_int, [_vp, _i64, _i64, _vp, _fp, _vp]),
+    "jq_w4a4_workspace_bytes": (_sz, [_i64, _i64]),
+    "jq_w4a4_linear": (ctypes.c_int, [_vp, _i64, _i64, _vp, _fp, _i64, _vp, _vp, _vp, _sz, _vp]),
+    "jq_w4a4_gemm": (ctypes.c_int, [_vp, _fp, _i64, _i64, _vp, _fp, _i64, _vp, _vp, _vp]),
+    "jq_w4a4_gemm_i32": (ctypes.c_int, [_vp, _i64, _i64, _vp, _i64, _ip, _vp]),
+}
+
+_lib = None
+
+
+class JQError(RuntimeError):
+    def __init__(self, status, where):
+        self.status = status
+        super().__init__(f"{where}: {jq_status_string(status)} ({status})")
+
+
+def lib():
+    """The loaded libjq.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(
+                f"{LIB_PATH} is missing: build the HIP library first "
+                "(python -c 'import __graft_entry__ as g; g.build()')")
+        l = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in SIGNATURES.items():
+            fn = getattr(l, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = l
+    return _lib
+
+
+def jq_status_string(status):
+    return lib().jq_status_string(int(status)).decode()
+
+
+def jq_version():
+    return lib().jq_version()
+
+
+def _check(status, where):
+    if status != JQ_OK:
+        raise JQError(status, where)
+
+
+def _torch():
+    import torch
+
+    return torch
+
+
+def _stream_ptr(stream):
+    torch = _torch()
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _dev(t, dtype, shape, name):
+    torch = _torch()
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must be on the GPU, got {t.device}")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def jq_w4a4_workspace_bytes(M, K):
+    return int(lib().jq_w4a4_workspace_bytes(int(M), int(K)))
+
+
+def jq_quantize_act(x, q=None, scale=None, stream=None):
+    """x bf16 [M,K] -> (q uint8 [M,K/2], scale fp32 [M])."""
+    torch = _torch()
+    M, K = x.shape
+    if q is None:
+        q = torch.empty((M, K // 2), dtype=torch.uint8, device=x.device)
+    if scale is None:
+        scale = torch.empty((M,), dtype=torch.float32, device=x.device)
+    st = lib().jq_quantize_act(_dev(x, torch.bfloat16, None, "x"), M, K,
+                               _dev(q, torch.uint8, (M, K // 2), "q"),
+                               _dev(scale, torch.float32, (M,), "scale"), _stream_ptr(stream))
+    _check(st, "jq_quantize_act")
+    return q, scale
+
+
+def jq_pack_weight_int4(w, wq=None, w_scale=None, stream=None):
+    """w bf16 [N,K] -> (wq uint8 [N,K/2], w_scale fp32 [N])."""
+    torch = _torch()
+    N, K = w.shape
+    if wq is None:
+        wq = torch.empty((N, K // 2), dtype=torch.uint8, device=w.device)
+    if w_scale is None:
+        w_scale = torch.empty((N,), dtype=torch.float32, device=w.device)
+    st = lib().jq_pack_weight_int4(_dev(w, torch.bfloat16, None, "w"), N, K,
+                                   _dev(wq, torch.uint8, (N, K // 2), "wq"),
+                                   _dev(w_scale, torch.float32, (N,), "w_scale"), _stream_ptr(stream))
+    _check(st, "jq_pack_weight_int4")
+    return wq, w_scale
+
+
+def jq_w4a4_linear(x, wq, w_scale, bias=None, y=None, workspace=None, stream=None):
+    """y = W4A4 linear of x (bf16 [M,K]) with a packed weight; returns bf16 [M,N]."""
+    torch = _torch()
+    M, K = x.shape
+    N = wq.shape[0]
+    if y is None:
+        y = torch.empty((M, N), dtype=torch.bfloat16, device=x.device)
+    need = jq_w4a4_workspace_bytes(M, K)
+    if workspace is None:
+        workspace = torch.empty((need,), dtype=torch.uint8, device=x.device)
+    bptr = ctypes.c_void_p(None) if bias is None else _dev(bias, torch.bfloat16, (N,), "bias")
+    st = lib().jq_w4a4_linear(_dev(x, torch.bfloat16, None, "x"), M, K,
+                              _dev(wq, torch.uint8, (N, K // 2), "wq"),
+                              _dev(w_scale, torch.float32, (N,), "w_scale"), N, bptr,
+                              _dev(y, torch.bfloat16, (M, N), "y"),
+                              _dev(workspace, torch.uint8, None, "workspace"),
+                              workspace.numel(), _stream_ptr(stream))
+    _check(st, "jq_w4a4_linear")
+    return y
+
+
+def jq_w4a4_gemm(q, scale, wq, w_scale, bias=None, y=None, stream=None):
+    """GEMM + epilogue on pre-quantised activations; returns bf16 [M,N]."""
+    torch = _torch()
+    M, Kh = q.shape
+    K = 2 * Kh
+    N = wq.shape[0]
+    if y is None:
+        y = torch.empty((M, N), dtype=torch.bfloat16, device=q.device)
+    bptr = ctypes.c_void_p(None) if bias is None else _dev(bias, torch.bfloat16, (N,), "bias")
+    st = lib().jq_w4a4_gemm(_dev(q, torch.uint8, (M, Kh), "q"), _dev(scale, torch.float32, (M,), "scale"),
+                            M, K, _dev(wq, torch.uint8, (N, Kh), "wq"),
+                            _dev(w_scale, torch.float32, (N,), "w_scale"), N, bptr,
+                            _dev(y, torch.bfloat16, (M, N), "y"), _stream_ptr(stream))
+    _check(st, "jq_w4a4_gemm")
+    return y
+
+
+def jq_w4a4_gemm_i32(q, wq, acc=None, stream=None):
+    """Exact accumulators int32 [M,N] of the packed codes."""
+    torch = _torch()
+    M, Kh = q.shape
+    N = wq.shape[0]
+    if acc is None:
+        acc = torch.empty((M, N), dtype=torch.int32, device=q.device)
+    st = lib().jq_w4a4_gemm_i32(_dev(q, torch.uint8, (M, Kh), "q"), M, 2 * Kh,
+                                _dev(wq, torch.uint8, (N, Kh), "wq"), N,
+                                _dev(acc, torch.int32, (M, N), "acc"), _stream_ptr(stream))
+    _check(st, "jq_w4a4_gemm_i32")
+    return acc
+
+
+# ---------------------------------------------------------------------------
+# host <-> device helpers for bf16 bit patterns (data movement only)
+# ---------------------------------------------------------------------------
+
+
+def bf16_tensor(bits, device="cuda"):
+    """numpy uint16 bf16 bit patterns -> torch.bfloat16 tensor on `device`."""
+    import numpy as np
+
+    torch = _torch()
+    t = torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16)
+    return t.to(device)
+
+
+def bf16_bits(t):
+    """torch.bfloat16 tensor -> numpy uint16 bit patterns (on the host)."""
+    import numpy as np
+
+    torch = _torch()
+    return t.detach().contiguous().view(torch.int16).cpu().numpy().view(np.uint16)

@@ -1,0 +1,120 @@
+"""C-ABI checks that need no GPU: the library loads, exports every symbol the
+header declares, and rejects bad arguments before launching anything.
+
+Only argument-validation paths are exercised here (fake device addresses are
+never dereferenced because every call below fails validation first).
+"""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2609_33601_amd import jq
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "jq.h")
+
+pytestmark = pytest.mark.skipif(not os.path.exists(jq.LIB_PATH),
+                                reason="libjq.so not built (run __graft_entry__.build())")
+
+A = 0x10000  # a fake, 256-byte-aligned address
+MIS = A + 2  # 2-byte aligned only
+
+
+def header_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(jq_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_exports_every_declared_symbol():
+    names = header_functions()
+    assert len(names) == 8, names
+    lib = ctypes.CDLL(jq.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), f"libjq.so does not export {n}"
+    assert set(names) == set(jq.SIGNATURES), "binding and header disagree"
+
+
+def test_status_strings_and_version():
+    assert jq.jq_status_string(0) == "JQ_OK"
+    assert jq.jq_status_string(4) == "JQ_ERR_WORKSPACE_TOO_SMALL"
+    assert jq.jq_status_string(99) == "JQ_ERR_UNKNOWN"
+    assert jq.jq_version() >= 100
+
+
+def test_workspace_bytes():
+    L = jq.lib()
+    assert L.jq_w4a4_workspace_bytes(4608, 3072) == 4608 * 1536 + 18432
+    assert L.jq_w4a4_workspace_bytes(1, 64) == 256 + 256
+    assert L.jq_w4a4_workspace_bytes(3, 128) == 256 + 256
+    assert L.jq_w4a4_workspace_bytes(0, 64) == 0
+    assert L.jq_w4a4_workspace_bytes(8, 100) == 0
+
+
+@pytest.mark.parametrize("fn", ["jq_quantize_act", "jq_pack_weight_int4"])
+def test_quantize_validation(fn):
+    f = getattr(jq.lib(), fn)
+    assert f(None, 8, 64, A, A, None) == jq.JQ_ERR_INVALID_ARG
+    assert f(A, 8, 64, None, A, None) == jq.JQ_ERR_INVALID_ARG
+    assert f(A, 8, 64, A, None, None) == jq.JQ_ERR_INVALID_ARG
+    assert f(A, 0, 64, A, A, None) == jq.JQ_ERR_INVALID_ARG
+    assert f(A, -3, 64, A, A, None) == jq.JQ_ERR_INVALID_ARG
+    assert f(A, 8, 0, A, A, None) == jq.JQ_ERR_INVALID_ARG
+    for K in (2, 32, 100, 65536 + 64):
+        assert f(A, 8, K, A, A, None) == jq.JQ_ERR_UNSUPPORTED_SHAPE, K
+    assert f(A, 1 << 31, 64, A, A, None) == jq.JQ_ERR_UNSUPPORTED_SHAPE
+    assert f(MIS, 8, 64, A, A, None) == jq.JQ_ERR_MISALIGNED
+    assert f(A, 8, 64, A + 8, A, None) == jq.JQ_ERR_MISALIGNED
+    assert f(A, 8, 64, A, A + 1, None) == jq.JQ_ERR_MISALIGNED
+
+
+def test_linear_validation():
+    f = jq.lib().jq_w4a4_linear
+    need = jq.lib().jq_w4a4_workspace_bytes(16, 128)
+    ok = dict(x=A, M=16, K=128, wq=A, sw=A, N=32, b=None, y=A, ws=A, wsb=need, s=None)
+
+    def call(**kw):
+        a = dict(ok)
+        a.update(kw)
+        return f(a["x"], a["M"], a["K"], a["wq"], a["sw"], a["N"], a["b"], a["y"], a["ws"], a["wsb"], a["s"])
+
+    for k in ("x", "wq", "sw", "y", "ws"):
+        assert call(**{k: None}) == jq.JQ_ERR_INVALID_ARG, k
+    assert call(M=0) == jq.JQ_ERR_INVALID_ARG
+    assert call(N=0) == jq.JQ_ERR_INVALID_ARG
+    assert call(K=96) == jq.JQ_ERR_UNSUPPORTED_SHAPE
+    assert call(x=MIS) == jq.JQ_ERR_MISALIGNED
+    assert call(wq=A + 4) == jq.JQ_ERR_MISALIGNED
+    assert call(y=A + 8) == jq.JQ_ERR_MISALIGNED
+    assert call(sw=A + 2) == jq.JQ_ERR_MISALIGNED
+    assert call(b=A + 1) == jq.JQ_ERR_MISALIGNED
+    assert call(ws=A + 16) == jq.JQ_ERR_MISALIGNED
+    assert call(wsb=need - 1) == jq.JQ_ERR_WORKSPACE_TOO_SMALL
+    assert call(wsb=0) == jq.JQ_ERR_WORKSPACE_TOO_SMALL
+
+
+def test_gemm_validation():
+    g = jq.lib().jq_w4a4_gemm
+    assert g(None, A, 4, 64, A, A, 4, None, A, None) == jq.JQ_ERR_INVALID_ARG
+    assert g(A, None, 4, 64, A, A, 4, None, A, None) == jq.JQ_ERR_INVALID_ARG
+    assert g(A, A, 4, 64, A, None, 4, None, A, None) == jq.JQ_ERR_INVALID_ARG
+    assert g(A, A, 4, 64, A, A, 4, None, None, None) == jq.JQ_ERR_INVALID_ARG
+    assert g(A, A, 4, 192 + 32, A, A, 4, None, A, None) == jq.JQ_ERR_UNSUPPORTED_SHAPE
+    assert g(A + 8, A, 4, 64, A, A, 4, None, A, None) == jq.JQ_ERR_MISALIGNED
+    i = jq.lib().jq_w4a4_gemm_i32
+    assert i(None, 4, 64, A, 4, A, None) == jq.JQ_ERR_INVALID_ARG
+    assert i(A, 4, 64, A, 4, None, None) == jq.JQ_ERR_INVALID_ARG
+    assert i(A, 4, 64, A, -1, A, None) == jq.JQ_ERR_INVALID_ARG
+    assert i(A, 4, 48, A, 4, A, None) == jq.JQ_ERR_UNSUPPORTED_SHAPE
+    assert i(A, 4, 64, A, 4, A + 4, None) == jq.JQ_ERR_MISALIGNED
+    assert i(A, 1 << 30, 64, A, 1 << 20, A, None) == jq.JQ_ERR_UNSUPPORTED_SHAPE
+
+
+def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
+    monkeypatch.setattr(jq, "_lib", None)
+    monkeypatch.setattr(jq, "LIB_PATH", str(tmp_path / "missing.so"))
+    with pytest.raises(RuntimeError, match="missing"):
+        jq.lib()
