@@ -40,7 +40,8 @@
  *   - Shapes: rows (M, N) >= 1; K >= 64 and K % 64 == 0, else
  *     JQ_ERR_UNSUPPORTED_SHAPE; K <= 65536 so that every accumulator stays
  *     exact in int32 and in fp32; rows <= 2^30 and, for the GEMM calls,
- *     ceil(M/256) * ceil(N/256) <= 2^26, else JQ_ERR_UNSUPPORTED_SHAPE.
+ *     ceil(M/256) * ceil(N/256) <= 2^26 and each packed operand (M*K/2 and
+ *     N*K/2 bytes) below 2 GiB, else JQ_ERR_UNSUPPORTED_SHAPE.
  *     Non-positive sizes or required NULL pointers give JQ_ERR_INVALID_ARG.
  *   - Matrix and packed pointers must be 16-byte aligned and scale/bias pointers
  *     4-/2-byte aligned, else JQ_ERR_MISALIGNED.

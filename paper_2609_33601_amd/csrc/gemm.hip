@@ -7,21 +7,32 @@
 // with every fp32 operation rounded on its own (built with -ffp-contract=off).
 //
 // Structure.
-//  * Block tile 256 (m) x 256 (n); four waves, each owning 128 x 128 outputs
-//    as an 8 x 8 grid of 16 x 16 MFMA tiles (256 int32 accumulators per lane).
-//  * K is consumed 128 codes (64 packed bytes per row) per stage.  Packed
-//    tiles are loaded from global memory with 16-byte loads into registers one
-//    stage ahead, then written to a double-buffered LDS tile (2 x 32 KiB).
-//    LDS rows are 64 bytes; the 16-byte chunk c of row r is stored at
-//    c ^ ((r >> 1) & 3) so that the 16 rows a lane group reads land on
-//    different banks.
-//  * Each MFMA v_mfma_i32_16x16x64_i8 consumes, per lane, 8 packed bytes of
-//    one row of each operand.  They are unpacked in registers without any
-//    sign extension: hi = p & 0xF0F0F0F0 and lo = (p << 4) & 0xF0F0F0F0 hold
+//  * Block tile 128 (m) x 256 (n), four waves of 64 x 128 outputs each (a
+//    4 x 8 grid of 16 x 16 MFMA tiles, 128 int32 accumulators per lane).  A
+//    block needs 48 KiB of LDS and at most 256 registers per lane, so two
+//    blocks share a CU and each SIMD runs two waves from different blocks:
+//    while one block waits at its barrier or on LDS, the other issues MFMAs.
+//  * K is consumed 128 codes (64 packed bytes per row) per stage; two stages
+//    alternate.  Tiles move from global memory straight into LDS with
+//    buffer_load_dwordx4 ... lds (no staging registers, no LDS write
+//    instructions), one stage ahead of the MFMAs.  The buffer form keeps the
+//    per-lane address a 32-bit offset next to a scalar descriptor.  LDS rows are 64 bytes; the
+//    16-byte chunk c of row r sits at slot c ^ ((r >> 1) & 3), realised by
+//    choosing, for each lane, the global chunk that belongs in its
+//    (lane-ordered) DMA slot.  A ds_read_b128 of one chunk per lane then
+//    spreads 8 consecutive lanes over 8 rows and all banks.
+//  * Each v_mfma_i32_16x16x64_i8 consumes, per lane, 8 packed bytes of one
+//    row of each operand: lane group g (lanes 16g..16g+15) takes 16-byte
+//    chunk g of its row, the first 8 bytes in the first half-stage and the
+//    last 8 in the second.  They are unpacked in registers without any sign
+//    extension: hi = p & 0xF0F0F0F0 and lo = (p << 4) & 0xF0F0F0F0 hold
 //    16 * code as int8.  Both operands are unpacked the same way, so the k
 //    order inside an MFMA is the same permutation for both and the sum is
 //    unchanged; the accumulator holds 256 * acc exactly (|256 * acc| <= 2^30
 //    for K <= 65536) and the epilogue shifts it back with >> 8.
+//  * Per stage: read this stage's fragments, start the DMA of the next stage,
+//    64 MFMAs, wait for the DMA, barrier.  No DMA is in flight when the
+//    fragments are read, so the reads never wait on it.
 //  * The weight tile is the MFMA A operand and the activation tile the B
 //    operand, so the result is y^T: each lane ends up with 4 consecutive
 //    output columns n of one row m, stored as one 8-byte bf16 write.
@@ -39,20 +50,28 @@ namespace jq {
 namespace {
 
 typedef int v4i __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) void lds_void_t;
 
-constexpr int kBM = 256;       // activation rows per block
+constexpr int kBM = 128;       // activation rows per block
 constexpr int kBN = 256;       // weight rows per block
 constexpr int kBKB = 64;       // packed bytes of K per stage (128 codes)
-constexpr int kChunks = kBKB / 16;  // 16-byte chunks per row per stage
+constexpr int kChunks = kBKB / 16;           // 16-byte chunks per row per stage
+constexpr int kXSlots = kBM * kChunks;       // 16-byte slots of the activation tile
+constexpr int kStageSlots = (kBM + kBN) * kChunks;
 constexpr int kThreads = 256;
-constexpr int kWM = 128, kWN = 128;  // per-wave tile
+constexpr int kWM = 64, kWN = 128;           // per-wave tile
 constexpr int kFM = kWM / 16, kFN = kWN / 16;
-constexpr int kGroupM = 4;
+constexpr int kXDma = kBM / 64;              // DMA instructions per wave per stage, activations
+constexpr int kWDma = kBN / 64;              // and weights (each fills 16 rows)
+constexpr int kGroupM = 8;
 constexpr int kNumXcd = 8;
+constexpr int kBufferFlags = 0x00020000;     // buffer descriptor word 3 for raw byte-addressed loads
+constexpr int kWaitVm0 = (0x7 << 4) | (0xF << 8);  // s_waitcnt vmcnt(0), other counters untouched
 
 static_assert(kChunks == 4, "swizzle below assumes 4 chunks per LDS row");
 
-__device__ __forceinline__ int swz(int row, int chunk) { return row * kChunks + (chunk ^ ((row >> 1) & 3)); }
+// LDS slot (16-byte units) of chunk c of tile row r.
+__device__ __forceinline__ int lds_slot(int row, int c) { return row * kChunks + (c ^ ((row >> 1) & 3)); }
 
 __device__ __forceinline__ v4i unpack8(uint32_t p0, uint32_t p1) {
   v4i r;
@@ -82,14 +101,17 @@ __device__ __forceinline__ bool tile_of_block(int bid, int tiles_m, int tiles_n,
   return true;
 }
 
-template <Epilogue EPI, bool HAS_BIAS>
-__global__ __launch_bounds__(kThreads, 1) void w4a4_gemm_kernel(
+template <Epilogue EPI, bool HAS_BIAS, bool KTAIL>
+__global__ __launch_bounds__(kThreads, 2) void w4a4_gemm_kernel(
     const uint8_t* __restrict__ qx, const float* __restrict__ sx, int M, int K,
     const uint8_t* __restrict__ qw, const float* __restrict__ sw, int N,
     const uint16_t* __restrict__ bias, void* __restrict__ out, int tiles_m, int tiles_n) {
-  __shared__ uint4 lds_x[2][kBM * kChunks];
-  __shared__ uint4 lds_w[2][kBN * kChunks];
+  // Two stage buffers, each the activation tile followed by the weight tile.
+  __shared__ uint4 lds0[kStageSlots];
+  __shared__ uint4 lds1[kStageSlots];
 
+  // Mark the function as using AGPRs so that MFMA accumulators are allocated
+  // there, leaving the architectural VGPRs to operands and addresses.
   TileCoord tc;
   if (!tile_of_block(blockIdx.x, tiles_m, tiles_n, &tc)) return;
   const int m0 = tc.tm * kBM;
@@ -97,42 +119,51 @@ __global__ __launch_bounds__(kThreads, 1) void w4a4_gemm_kernel(
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform, held in an SGPR
+  const int wm = wave & 1, wn = wave >> 1;
   const int li = lane & 15, lg = lane >> 4;
 
   const int64_t row_bytes = K / 2;
   const int ksteps = static_cast<int>((row_bytes + kBKB - 1) / kBKB);
 
-  // Global -> register staging: thread loads chunk (tid & 3) of rows (tid >> 2) + 64 i.
-  const int ld_chunk = tid & 3;
-  const int ld_row = tid >> 2;
-  const uint8_t* gx[4];
-  const uint8_t* gw[4];
+  // DMA pattern: one instruction fills 16 tile rows R .. R + 15, i.e. LDS
+  // slots 4R .. 4R + 63 in lane order.  Lane l lands in slot 4R + l = row
+  // R + (l >> 2), swizzled chunk l & 3, so it fetches global chunk
+  // (l & 3) ^ ((row >> 1) & 3) = (l & 3) ^ ((l >> 3) & 3).
+  // Byte offsets within each operand fit in 32 bits (checked by the host),
+  // so the DMA uses a scalar base plus one 32-bit offset per lane.
+  const int dma_chunk = (lane & 3) ^ ((lane >> 3) & 3);
+  uint32_t ox[kXDma], ow[kWDma];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int rx = min(m0 + ld_row + 64 * i, M - 1);
-    const int rw = min(n0 + ld_row + 64 * i, N - 1);
-    gx[i] = qx + static_cast<int64_t>(rx) * row_bytes + ld_chunk * 16;
-    gw[i] = qw + static_cast<int64_t>(rw) * row_bytes + ld_chunk * 16;
+  for (int j = 0; j < kXDma; ++j) {
+    const int r = 16 * (kXDma * wave + j) + (lane >> 2);
+    ox[j] = static_cast<uint32_t>(min(m0 + r, M - 1)) * static_cast<uint32_t>(row_bytes) + 16 * dma_chunk;
   }
-  uint4 stx[4], stw[4];
+#pragma unroll
+  for (int j = 0; j < kWDma; ++j) {
+    const int r = 16 * (kWDma * wave + j) + (lane >> 2);
+    ow[j] = static_cast<uint32_t>(min(n0 + r, N - 1)) * static_cast<uint32_t>(row_bytes) + 16 * dma_chunk;
+  }
 
-  auto load_stage = [&](int ks) {
-    const int64_t kb = static_cast<int64_t>(ks) * kBKB;
-    const bool ok = kb + ld_chunk * 16 < row_bytes;
+  // Buffer descriptors over the two packed operands (sizes < 2^31, checked by the host).
+  const __amdgpu_buffer_rsrc_t rsx =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(qx), 0, static_cast<int>(M * row_bytes), kBufferFlags);
+  const __amdgpu_buffer_rsrc_t rsw =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(qw), 0, static_cast<int>(N * row_bytes), kBufferFlags);
+
+  auto issue = [&](uint4* buf, int ks) {
+    const int kb = ks * kBKB;
+    // Last stage of a K % 128 == 64 problem: chunks 2 and 3 lie past the row
+    // end; fetch an in-bounds chunk instead, the fragment read zeroes them.
+    const uint32_t back = (KTAIL && kb + 16 * dma_chunk >= row_bytes) ? 32u : 0u;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      stx[i] = ok ? *reinterpret_cast<const uint4*>(gx[i] + kb) : make_uint4(0, 0, 0, 0);
-      stw[i] = ok ? *reinterpret_cast<const uint4*>(gw[i] + kb) : make_uint4(0, 0, 0, 0);
-    }
-  };
-  auto store_stage = [&](int buf) {
+    for (int j = 0; j < kXDma; ++j)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsx, (lds_void_t*)(buf + 64 * (kXDma * wave + j)), 16, ox[j] - back,
+                                               kb, 0, 0);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      lds_x[buf][swz(ld_row + 64 * i, ld_chunk)] = stx[i];
-      lds_w[buf][swz(ld_row + 64 * i, ld_chunk)] = stw[i];
-    }
+    for (int j = 0; j < kWDma; ++j)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsw, (lds_void_t*)(buf + kXSlots + 64 * (kWDma * wave + j)), 16,
+                                               ow[j] - back, kb, 0, 0);
   };
 
   v4i acc[kFN][kFM];
@@ -141,24 +172,24 @@ __global__ __launch_bounds__(kThreads, 1) void w4a4_gemm_kernel(
 #pragma unroll
     for (int b = 0; b < kFM; ++b) acc[a][b] = v4i{0, 0, 0, 0};
 
-  load_stage(0);
-  store_stage(0);
-  __syncthreads();
-
-  for (int ks = 0; ks < ksteps; ++ks) {
-    const int buf = ks & 1;
-    if (ks + 1 < ksteps) load_stage(ks + 1);
-
-    // This lane's 16 packed bytes (chunk lg) of each fragment row; the first 8
-    // bytes feed the first MFMA k-step of the stage, the last 8 the second.
+  // One stage: read fragments from `cur`, start the DMA of stage ks + 1 into
+  // `nxt`, run both MFMA half-stages, wait for the DMA and barrier.
+  auto stage = [&](const uint4* cur, uint4* nxt, int ks) {
     uint4 pw[kFN], px[kFM];
 #pragma unroll
-    for (int f = 0; f < kFN; ++f) pw[f] = lds_w[buf][swz(kWN * wn + 16 * f + li, lg)];
+    for (int f = 0; f < kFN; ++f) pw[f] = cur[kXSlots + lds_slot(kWN * wn + 16 * f + li, lg)];
 #pragma unroll
-    for (int f = 0; f < kFM; ++f) px[f] = lds_x[buf][swz(kWM * wm + 16 * f + li, lg)];
-
+    for (int f = 0; f < kFM; ++f) px[f] = cur[lds_slot(kWM * wm + 16 * f + li, lg)];
+    if (KTAIL && ks == ksteps - 1 && lg >= 2) {
+#pragma unroll
+      for (int f = 0; f < kFN; ++f) pw[f] = make_uint4(0, 0, 0, 0);
+#pragma unroll
+      for (int f = 0; f < kFM; ++f) px[f] = make_uint4(0, 0, 0, 0);
+    }
+    if (ks + 1 < ksteps) issue(nxt, ks + 1);
 #pragma unroll
     for (int kk = 0; kk < 2; ++kk) {
+      __builtin_amdgcn_sched_barrier(0);
       v4i bx[kFM];
 #pragma unroll
       for (int f = 0; f < kFM; ++f) bx[f] = kk == 0 ? unpack8(px[f].x, px[f].y) : unpack8(px[f].z, px[f].w);
@@ -170,10 +201,20 @@ __global__ __launch_bounds__(kThreads, 1) void w4a4_gemm_kernel(
           acc[fn][fm] = __builtin_amdgcn_mfma_i32_16x16x64_i8(aw, bx[fm], acc[fn][fm], 0, 0, 0);
       }
     }
-
-    if (ks + 1 < ksteps) store_stage(buf ^ 1);
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_waitcnt(kWaitVm0);
     __syncthreads();
+  };
+
+  issue(lds0, 0);
+  __builtin_amdgcn_s_waitcnt(kWaitVm0);
+  __syncthreads();
+  int ks = 0;
+  for (; ks + 2 <= ksteps; ks += 2) {
+    stage(lds0, lds1, ks);
+    stage(lds1, lds0, ks + 1);
   }
+  if (ks < ksteps) stage(lds0, lds1, ks);
 
   // Epilogue.  Lane holds, for tile (fn, fm), rows n = nb + 4 lg + r (r = 0..3)
   // of column m = mb + li of y^T.
@@ -256,16 +297,18 @@ hipError_t launch_w4a4_gemm(Epilogue epi, const uint8_t* qx, const float* sx, in
   const dim3 grid(static_cast<unsigned>(per_xcd * kNumXcd));
   const dim3 block(kThreads);
   const int Mi = static_cast<int>(M), Ki = static_cast<int>(K), Ni = static_cast<int>(N);
+  const bool tail = (K % 128) != 0;
+#define JQ_LAUNCH(E, B, T)                                                                      \
+  hipLaunchKernelGGL((w4a4_gemm_kernel<E, B, T>), grid, block, 0, st, qx, sx, Mi, Ki, qw, sw, Ni, \
+                     bias, out, tiles_m, tiles_n)
   if (epi == Epilogue::kInt32) {
-    hipLaunchKernelGGL((w4a4_gemm_kernel<Epilogue::kInt32, false>), grid, block, 0, st, qx, sx, Mi,
-                       Ki, qw, sw, Ni, bias, out, tiles_m, tiles_n);
+    if (tail) JQ_LAUNCH(Epilogue::kInt32, false, true); else JQ_LAUNCH(Epilogue::kInt32, false, false);
   } else if (bias != nullptr) {
-    hipLaunchKernelGGL((w4a4_gemm_kernel<Epilogue::kBf16, true>), grid, block, 0, st, qx, sx, Mi,
-                       Ki, qw, sw, Ni, bias, out, tiles_m, tiles_n);
+    if (tail) JQ_LAUNCH(Epilogue::kBf16, true, true); else JQ_LAUNCH(Epilogue::kBf16, true, false);
   } else {
-    hipLaunchKernelGGL((w4a4_gemm_kernel<Epilogue::kBf16, false>), grid, block, 0, st, qx, sx, Mi,
-                       Ki, qw, sw, Ni, bias, out, tiles_m, tiles_n);
+    if (tail) JQ_LAUNCH(Epilogue::kBf16, false, true); else JQ_LAUNCH(Epilogue::kBf16, false, false);
   }
+#undef JQ_LAUNCH
   return hipGetLastError();
 }
 

@@ -44,8 +44,10 @@ jq_status check_gemm(const void* qx, const float* sx, int64_t M, int64_t K, cons
   if (st != JQ_OK) return st;
   st = check_shape(N, K);
   if (st != JQ_OK) return st;
-  // The tile grid is indexed with 32-bit integers.
+  // The tile grid is indexed with 32-bit integers, and each packed operand is
+  // addressed through a buffer descriptor with a 31-bit size.
   if (((M + 255) / 256) * ((N + 255) / 256) > (int64_t(1) << 26)) return JQ_ERR_UNSUPPORTED_SHAPE;
+  if (M * (K / 2) >= (int64_t(1) << 31) || N * (K / 2) >= (int64_t(1) << 31)) return JQ_ERR_UNSUPPORTED_SHAPE;
   if (!aligned(qx, 16) || !aligned(qw, 16) || !aligned(y, 16)) return JQ_ERR_MISALIGNED;
   if ((sx != nullptr && !aligned(sx, 4)) || (sw != nullptr && !aligned(sw, 4))) return JQ_ERR_MISALIGNED;
   if (bias != nullptr && !aligned(bias, 2)) return JQ_ERR_MISALIGNED;

@@ -111,6 +111,7 @@ def test_gemm_validation():
     assert i(A, 4, 48, A, 4, A, None) == jq.JQ_ERR_UNSUPPORTED_SHAPE
     assert i(A, 4, 64, A, 4, A + 4, None) == jq.JQ_ERR_MISALIGNED
     assert i(A, 1 << 30, 64, A, 1 << 20, A, None) == jq.JQ_ERR_UNSUPPORTED_SHAPE
+    assert i(A, 1 << 20, 4096, A, 64, A, None) == jq.JQ_ERR_UNSUPPORTED_SHAPE  # 2 GiB packed activations
 
 
 def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
