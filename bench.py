@@ -36,7 +36,31 @@ def parse_args():
     p.add_argument("--warmup", type=int, default=20)
     p.add_argument("--no-cpu-baseline", action="store_true", help="skip the oracle CPU baseline leg")
     p.add_argument("--cpu-seconds", type=float, default=12.0, help="target CPU time of the oracle sample")
+    p.add_argument("--copy-calib", action="store_true",
+                   help="also run a plain 256 MiB device copy (calibrates HBM byte counters under rocprofv3)")
     return p.parse_args()
+
+
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_flux_mlp.json")
+GEMM_SOURCE = os.path.join(ROOT, "paper_2609_33601_amd", "csrc", "gemm.hip")
+
+
+def recorded_traffic(kernel_linear):
+    """HBM bytes per launch of the dominant kernel from the committed counter
+    runs, or None if there are none or the kernel source changed since."""
+    import hashlib
+
+    try:
+        rec = json.load(open(TRAFFIC_FILE))
+        sha = hashlib.sha256(open(GEMM_SOURCE, "rb").read()).hexdigest()
+    except (OSError, ValueError):
+        return None
+    if rec.get("gemm_source_sha256") != sha:
+        return None
+    k = rec.get("kernels", {}).get(kernel_linear)
+    if not k:
+        return None
+    return k["fetch_bytes"] + k["write_bytes"]
 
 
 def log(*a):
@@ -189,6 +213,17 @@ def main():
     roofline = {"bound": "mfma", "achieved": dom["achieved_TOPS"], "peak": PEAK_INT8_TOPS, "unit": "TOP/s",
                 "frac": dom["achieved_TOPS"] / PEAK_INT8_TOPS, "traffic": None,
                 "kernel": f"w4a4_gemm ({dom['linear']})", "avg_launch_us": dom["avg_us"]}
+
+    roofline["traffic"] = recorded_traffic(dom["linear"])
+
+    if args.copy_calib:
+        # Reference for FETCH_SIZE / WRITE_SIZE: a plain device copy of 256 MiB.
+        src = torch.empty(256 << 20, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     # Re-run the timed configuration once so that y holds the linear's outputs for the parity sample.
     step()

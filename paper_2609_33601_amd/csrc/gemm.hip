@@ -9,30 +9,42 @@
 // Structure.
 //  * Block tile 128 (m) x 256 (n), four waves of 64 x 128 outputs each (a
 //    4 x 8 grid of 16 x 16 MFMA tiles, 128 int32 accumulators per lane).  A
-//    block needs 48 KiB of LDS and at most 256 registers per lane, so two
+//    block needs 64 KiB of LDS and at most 256 registers per lane, so two
 //    blocks share a CU and each SIMD runs two waves from different blocks:
 //    while one block waits at its barrier or on LDS, the other issues MFMAs.
-//  * K is consumed 128 codes (64 packed bytes per row) per stage; two stages
-//    alternate.  Tiles move from global memory straight into LDS with
-//    buffer_load_dwordx4 ... lds (no staging registers, no LDS write
-//    instructions), one stage ahead of the MFMAs.  The buffer form keeps the
-//    per-lane address a 32-bit offset next to a scalar descriptor.  LDS rows are 64 bytes; the
-//    16-byte chunk c of row r sits at slot c ^ ((r >> 1) & 3), realised by
-//    choosing, for each lane, the global chunk that belongs in its
-//    (lane-ordered) DMA slot.  A ds_read_b128 of one chunk per lane then
-//    spreads 8 consecutive lanes over 8 rows and all banks.
-//  * Each v_mfma_i32_16x16x64_i8 consumes, per lane, 8 packed bytes of one
-//    row of each operand: lane group g (lanes 16g..16g+15) takes 16-byte
-//    chunk g of its row, the first 8 bytes in the first half-stage and the
-//    last 8 in the second.  They are unpacked in registers without any sign
-//    extension: hi = p & 0xF0F0F0F0 and lo = (p << 4) & 0xF0F0F0F0 hold
-//    16 * code as int8.  Both operands are unpacked the same way, so the k
-//    order inside an MFMA is the same permutation for both and the sum is
-//    unchanged; the accumulator holds 256 * acc exactly (|256 * acc| <= 2^30
-//    for K <= 65536) and the epilogue shifts it back with >> 8.
-//  * Per stage: read this stage's fragments, start the DMA of the next stage,
-//    64 MFMAs, wait for the DMA, barrier.  No DMA is in flight when the
-//    fragments are read, so the reads never wait on it.
+//  * gfx950 has no int4 MFMA, so codes are widened to int8 for
+//    v_mfma_i32_16x16x64_i8.  Widening is VALU work, and VALU instructions
+//    between MFMAs slow the matrix pipe of the SIMD (measured with two waves
+//    per SIMD: 1.5 and 2.25 VALU per MFMA cost 16% and 34% of the MFMA rate).
+//    The activation tile is therefore widened once per block: it is loaded
+//    into registers, widened, and written to LDS as int8, and the waves read
+//    ready-to-use operands.  The weight tile (twice as many rows) stays packed
+//    in LDS and each wave widens its own fragments.  That is ~1.7 VALU per
+//    MFMA instead of 2.25, within the LDS budget of two blocks per CU.
+//  * Widening without sign extension: hi = p & 0xF0F0F0F0 and
+//    lo = (p << 4) & 0xF0F0F0F0 hold 16 * code as int8.  A packed dword of
+//    codes k0..k7 becomes [k0 k2 k4 k6] and [k1 k3 k5 k7]; both operands are
+//    widened in the same order, so every MFMA sees the same k permutation on
+//    A and B and the sum is unchanged.  The accumulator holds 256 * acc
+//    exactly (|256 * acc| <= 2^30 for K <= 65536); the epilogue shifts back.
+//  * K is consumed 128 codes (64 packed bytes per row) per stage, two stages
+//    alternating.  The weight tile moves from global memory straight into LDS
+//    with buffer_load_dwordx4 ... lds (no staging registers, no LDS write
+//    instructions), one stage ahead.  Weight LDS rows are 64 bytes: 16-byte
+//    chunk c of row r sits at slot c ^ ((r >> 1) & 3), realised by choosing,
+//    for each lane, the global chunk that belongs in its (lane-ordered) DMA
+//    slot.  Activation LDS rows are 128 bytes of int8: chunk c of row r sits
+//    at c ^ (r & 7).  Either way a ds_read_b128 of one chunk per lane spreads
+//    8 consecutive lanes over 8 rows and all banks.
+//  * Lane group g (lanes 16g..16g+15) takes, in MFMA half-stage h, codes
+//    32g + 16h .. 32g + 16h + 15 of its row: bytes 8h..8h+7 of packed weight
+//    chunk g, and int8 activation chunk 2g + h.
+//  * Per stage: read this stage's fragments, start the weight DMA and the
+//    activation loads of the next stage, 64 MFMAs (each weight fragment is
+//    widened just before its four MFMAs), wait, widen and write the next
+//    activation tile, barrier.  The loop body is one stage over a
+//    parity-selected LDS buffer (no unrolling), which keeps the register
+//    allocation free of rotating copies.
 //  * The weight tile is the MFMA A operand and the activation tile the B
 //    operand, so the result is y^T: each lane ends up with 4 consecutive
 //    output columns n of one row m, stored as one 8-byte bf16 write.
@@ -55,23 +67,27 @@ typedef __attribute__((address_space(3))) void lds_void_t;
 constexpr int kBM = 128;       // activation rows per block
 constexpr int kBN = 256;       // weight rows per block
 constexpr int kBKB = 64;       // packed bytes of K per stage (128 codes)
-constexpr int kChunks = kBKB / 16;           // 16-byte chunks per row per stage
-constexpr int kXSlots = kBM * kChunks;       // 16-byte slots of the activation tile
-constexpr int kStageSlots = (kBM + kBN) * kChunks;
+constexpr int kChunks = kBKB / 16;           // 16-byte packed chunks per row per stage
+constexpr int kXChunks = 2 * kChunks;        // 16-byte int8 chunks per activation row per stage
+constexpr int kXSlots = kBM * kXChunks;      // 16-byte slots of the int8 activation tile
+constexpr int kStageSlots = kXSlots + kBN * kChunks;
 constexpr int kThreads = 256;
-constexpr int kWM = 64, kWN = 128;           // per-wave tile
+constexpr int kWM = 128, kWN = 64;           // per-wave tile: all activation rows, a quarter of the weight rows
 constexpr int kFM = kWM / 16, kFN = kWN / 16;
-constexpr int kXDma = kBM / 64;              // DMA instructions per wave per stage, activations
-constexpr int kWDma = kBN / 64;              // and weights (each fills 16 rows)
+constexpr int kXLoads = kBM * kChunks / kThreads;  // 16-byte activation loads per thread per stage
+constexpr int kWDma = kBN / 64;              // weight DMA instructions per wave per stage (16 rows each)
 constexpr int kGroupM = 8;
 constexpr int kNumXcd = 8;
 constexpr int kBufferFlags = 0x00020000;     // buffer descriptor word 3 for raw byte-addressed loads
 constexpr int kWaitVm0 = (0x7 << 4) | (0xF << 8);  // s_waitcnt vmcnt(0), other counters untouched
 
-static_assert(kChunks == 4, "swizzle below assumes 4 chunks per LDS row");
+static_assert(kChunks == 4 && kXChunks == 8, "swizzles below assume 4 packed / 8 int8 chunks per LDS row");
+static_assert(kXLoads == 2, "activation staging below assumes two loads per thread");
 
-// LDS slot (16-byte units) of chunk c of tile row r.
-__device__ __forceinline__ int lds_slot(int row, int c) { return row * kChunks + (c ^ ((row >> 1) & 3)); }
+// LDS slots (16-byte units): chunk c of packed weight row r, and int8 chunk c
+// of activation row r.
+__device__ __forceinline__ int w_slot(int row, int c) { return row * kChunks + (c ^ ((row >> 1) & 3)); }
+__device__ __forceinline__ int x_slot(int row, int c) { return row * kXChunks + (c ^ (row & 7)); }
 
 __device__ __forceinline__ v4i unpack8(uint32_t p0, uint32_t p1) {
   v4i r;
@@ -106,12 +122,9 @@ __global__ __launch_bounds__(kThreads, 2) void w4a4_gemm_kernel(
     const uint8_t* __restrict__ qx, const float* __restrict__ sx, int M, int K,
     const uint8_t* __restrict__ qw, const float* __restrict__ sw, int N,
     const uint16_t* __restrict__ bias, void* __restrict__ out, int tiles_m, int tiles_n) {
-  // Two stage buffers, each the activation tile followed by the weight tile.
-  __shared__ uint4 lds0[kStageSlots];
-  __shared__ uint4 lds1[kStageSlots];
+  // Two stage buffers, each the int8 activation tile followed by the packed weight tile.
+  __shared__ uint4 lds[2 * kStageSlots];
 
-  // Mark the function as using AGPRs so that MFMA accumulators are allocated
-  // there, leaving the architectural VGPRs to operands and addresses.
   TileCoord tc;
   if (!tile_of_block(blockIdx.x, tiles_m, tiles_n, &tc)) return;
   const int m0 = tc.tm * kBM;
@@ -120,50 +133,65 @@ __global__ __launch_bounds__(kThreads, 2) void w4a4_gemm_kernel(
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform, held in an SGPR
-  const int wm = wave & 1, wn = wave >> 1;
+  const int wn = wave;  // waves split the weight rows; each covers every activation row
   const int li = lane & 15, lg = lane >> 4;
 
   const int64_t row_bytes = K / 2;
   const int ksteps = static_cast<int>((row_bytes + kBKB - 1) / kBKB);
 
-  // DMA pattern: one instruction fills 16 tile rows R .. R + 15, i.e. LDS
-  // slots 4R .. 4R + 63 in lane order.  Lane l lands in slot 4R + l = row
-  // R + (l >> 2), swizzled chunk l & 3, so it fetches global chunk
-  // (l & 3) ^ ((row >> 1) & 3) = (l & 3) ^ ((l >> 3) & 3).
-  // Byte offsets within each operand fit in 32 bits (checked by the host),
-  // so the DMA uses a scalar base plus one 32-bit offset per lane.
-  const int dma_chunk = (lane & 3) ^ ((lane >> 3) & 3);
-  uint32_t ox[kXDma], ow[kWDma];
-#pragma unroll
-  for (int j = 0; j < kXDma; ++j) {
-    const int r = 16 * (kXDma * wave + j) + (lane >> 2);
-    ox[j] = static_cast<uint32_t>(min(m0 + r, M - 1)) * static_cast<uint32_t>(row_bytes) + 16 * dma_chunk;
-  }
-#pragma unroll
-  for (int j = 0; j < kWDma; ++j) {
-    const int r = 16 * (kWDma * wave + j) + (lane >> 2);
-    ow[j] = static_cast<uint32_t>(min(n0 + r, N - 1)) * static_cast<uint32_t>(row_bytes) + 16 * dma_chunk;
-  }
-
-  // Buffer descriptors over the two packed operands (sizes < 2^31, checked by the host).
+  // Buffer descriptors over the two packed operands (sizes < 2^31, checked by
+  // the host), so every per-lane address is a 32-bit offset.
   const __amdgpu_buffer_rsrc_t rsx =
       __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(qx), 0, static_cast<int>(M * row_bytes), kBufferFlags);
   const __amdgpu_buffer_rsrc_t rsw =
       __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(qw), 0, static_cast<int>(N * row_bytes), kBufferFlags);
 
+  // Weight DMA: one instruction fills 16 tile rows R .. R + 15, i.e. LDS slots
+  // 4R .. 4R + 63 in lane order.  Lane l lands in slot 4R + l = row R + (l >> 2),
+  // swizzled chunk l & 3, so it fetches global chunk (l & 3) ^ ((l >> 3) & 3).
+  const int dma_chunk = (lane & 3) ^ ((lane >> 3) & 3);
+  uint32_t ow[kWDma];
+#pragma unroll
+  for (int j = 0; j < kWDma; ++j) {
+    const int r = 16 * (kWDma * wave + j) + (lane >> 2);
+    ow[j] = static_cast<uint32_t>(min(n0 + r, N - 1)) * static_cast<uint32_t>(row_bytes) + 16 * dma_chunk;
+  }
+  // Activation loads: thread loads packed chunk (tid & 3) of tile rows
+  // (tid >> 2) + 64 i; it widens chunk c into int8 chunks 2c and 2c + 1.
+  const int xl_chunk = tid & 3;
+  const int xl_row = tid >> 2;
+  uint32_t ox[kXLoads];
+#pragma unroll
+  for (int i = 0; i < kXLoads; ++i)
+    ox[i] = static_cast<uint32_t>(min(m0 + xl_row + 64 * i, M - 1)) * static_cast<uint32_t>(row_bytes) +
+            16 * xl_chunk;
+
+  uint4 gx[kXLoads];
   auto issue = [&](uint4* buf, int ks) {
     const int kb = ks * kBKB;
-    // Last stage of a K % 128 == 64 problem: chunks 2 and 3 lie past the row
-    // end; fetch an in-bounds chunk instead, the fragment read zeroes them.
+    // K % 128 == 64: in the last stage packed chunks 2 and 3 lie past the row
+    // end.  The weight DMA then fetches an in-bounds chunk instead; the
+    // activation codes there are zeroed, so those products vanish.
     const uint32_t back = (KTAIL && kb + 16 * dma_chunk >= row_bytes) ? 32u : 0u;
-#pragma unroll
-    for (int j = 0; j < kXDma; ++j)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsx, (lds_void_t*)(buf + 64 * (kXDma * wave + j)), 16, ox[j] - back,
-                                               kb, 0, 0);
 #pragma unroll
     for (int j = 0; j < kWDma; ++j)
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rsw, (lds_void_t*)(buf + kXSlots + 64 * (kWDma * wave + j)), 16,
                                                ow[j] - back, kb, 0, 0);
+#pragma unroll
+    for (int i = 0; i < kXLoads; ++i)
+      gx[i] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rsx, ox[i], kb, 0));
+    if (KTAIL && kb + 16 * xl_chunk >= row_bytes) {
+#pragma unroll
+      for (int i = 0; i < kXLoads; ++i) gx[i] = make_uint4(0, 0, 0, 0);
+    }
+  };
+  auto store_x = [&](uint4* buf) {
+#pragma unroll
+    for (int i = 0; i < kXLoads; ++i) {
+      const int row = xl_row + 64 * i;
+      buf[x_slot(row, 2 * xl_chunk)] = __builtin_bit_cast(uint4, unpack8(gx[i].x, gx[i].y));
+      buf[x_slot(row, 2 * xl_chunk + 1)] = __builtin_bit_cast(uint4, unpack8(gx[i].z, gx[i].w));
+    }
   };
 
   v4i acc[kFN][kFM];
@@ -172,53 +200,66 @@ __global__ __launch_bounds__(kThreads, 2) void w4a4_gemm_kernel(
 #pragma unroll
     for (int b = 0; b < kFM; ++b) acc[a][b] = v4i{0, 0, 0, 0};
 
-  // One stage: read fragments from `cur`, start the DMA of stage ks + 1 into
-  // `nxt`, run both MFMA half-stages, wait for the DMA and barrier.
+  // One stage: read fragments from `cur`, start the loads of stage ks + 1
+  // into `nxt`, run both MFMA half-stages, wait, write the widened activation
+  // tile of stage ks + 1, barrier.
   auto stage = [&](const uint4* cur, uint4* nxt, int ks) {
-    uint4 pw[kFN], px[kFM];
+    uint4 pw[kFN];
+    v4i bx0[kFM], bx1[kFM];
 #pragma unroll
-    for (int f = 0; f < kFN; ++f) pw[f] = cur[kXSlots + lds_slot(kWN * wn + 16 * f + li, lg)];
+    for (int f = 0; f < kFN; ++f) pw[f] = cur[kXSlots + w_slot(kWN * wn + 16 * f + li, lg)];
 #pragma unroll
-    for (int f = 0; f < kFM; ++f) px[f] = cur[lds_slot(kWM * wm + 16 * f + li, lg)];
-    if (KTAIL && ks == ksteps - 1 && lg >= 2) {
+    for (int f = 0; f < kFM; ++f) bx0[f] = __builtin_bit_cast(v4i, cur[x_slot(16 * f + li, 2 * lg)]);
 #pragma unroll
-      for (int f = 0; f < kFN; ++f) pw[f] = make_uint4(0, 0, 0, 0);
+    for (int f = 0; f < kFM; ++f) bx1[f] = __builtin_bit_cast(v4i, cur[x_slot(16 * f + li, 2 * lg + 1)]);
+    const bool more = ks + 1 < ksteps;
+    if (more) issue(nxt, ks + 1);
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-      for (int f = 0; f < kFM; ++f) px[f] = make_uint4(0, 0, 0, 0);
+    for (int fn = 0; fn < kFN; ++fn) {
+      const v4i aw = unpack8(pw[fn].x, pw[fn].y);
+#pragma unroll
+      for (int fm = 0; fm < kFM; ++fm)
+        acc[fn][fm] = __builtin_amdgcn_mfma_i32_16x16x64_i8(aw, bx0[fm], acc[fn][fm], 0, 0, 0);
     }
-    if (ks + 1 < ksteps) issue(nxt, ks + 1);
+    // Widen each weight fragment just before its row of MFMAs.
 #pragma unroll
-    for (int kk = 0; kk < 2; ++kk) {
-      __builtin_amdgcn_sched_barrier(0);
-      v4i bx[kFM];
+    for (int fn = 0; fn < kFN; ++fn) {
+      __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, kFM, 0);
+    }
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-      for (int f = 0; f < kFM; ++f) bx[f] = kk == 0 ? unpack8(px[f].x, px[f].y) : unpack8(px[f].z, px[f].w);
+    for (int fn = 0; fn < kFN; ++fn) {
+      const v4i aw = unpack8(pw[fn].z, pw[fn].w);
 #pragma unroll
-      for (int fn = 0; fn < kFN; ++fn) {
-        const v4i aw = kk == 0 ? unpack8(pw[fn].x, pw[fn].y) : unpack8(pw[fn].z, pw[fn].w);
+      for (int fm = 0; fm < kFM; ++fm)
+        acc[fn][fm] = __builtin_amdgcn_mfma_i32_16x16x64_i8(aw, bx1[fm], acc[fn][fm], 0, 0, 0);
+    }
+    // Widen each weight fragment just before its four MFMAs.
 #pragma unroll
-        for (int fm = 0; fm < kFM; ++fm)
-          acc[fn][fm] = __builtin_amdgcn_mfma_i32_16x16x64_i8(aw, bx[fm], acc[fn][fm], 0, 0, 0);
-      }
+    for (int fn = 0; fn < kFN; ++fn) {
+      __builtin_amdgcn_sched_group_barrier(0x002, 6, 1);
+      __builtin_amdgcn_sched_group_barrier(0x008, 4, 1);
     }
     __builtin_amdgcn_sched_barrier(0);
     __builtin_amdgcn_s_waitcnt(kWaitVm0);
+    if (more) store_x(nxt);
     __syncthreads();
   };
 
-  issue(lds0, 0);
+  issue(lds, 0);
   __builtin_amdgcn_s_waitcnt(kWaitVm0);
+  store_x(lds);
   __syncthreads();
-  int ks = 0;
-  for (; ks + 2 <= ksteps; ks += 2) {
-    stage(lds0, lds1, ks);
-    stage(lds1, lds0, ks + 1);
+  for (int ks = 0; ks < ksteps; ++ks) {
+    const int cur = (ks & 1) * kStageSlots;
+    stage(lds + cur, lds + (kStageSlots - cur), ks);
   }
-  if (ks < ksteps) stage(lds0, lds1, ks);
 
   // Epilogue.  Lane holds, for tile (fn, fm), rows n = nb + 4 lg + r (r = 0..3)
   // of column m = mb + li of y^T.
-  const int mb = m0 + kWM * wm + li;
+  const int mb = m0 + li;
   const int nb = n0 + kWN * wn + 4 * lg;
   const bool full = (m0 + kBM <= M) && (n0 + kBN <= N) && (N % 4 == 0);
 

@@ -102,13 +102,17 @@ __device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
   return v;
 }
 
+// One block per row: W = blockDim.x / 64 waves share the row, wave w owning
+// chunks w*NC .. w*NC + NC - 1 (chunk c = elements [c*512, c*512 + 512)).
 template <int NC>
-__global__ __launch_bounds__(256) void quantize_rows_kernel(
+__global__ __launch_bounds__(512) void quantize_rows_kernel(
     const uint16_t* __restrict__ x, int64_t M, int64_t K,
     uint8_t* __restrict__ q, float* __restrict__ scale) {
+  __shared__ uint32_t wave_max[8];
   const int lane = threadIdx.x & 63;
-  const int64_t row = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
-  if (row >= M) return;  // whole wave exits together
+  const int wave = threadIdx.x >> 6;
+  const int nwaves = blockDim.x >> 6;
+  const int64_t row = blockIdx.x;
 
   const uint16_t* xr = x + row * K;
   uint8_t* qr = q + row * (K / 2);
@@ -117,7 +121,7 @@ __global__ __launch_bounds__(256) void quantize_rows_kernel(
   u16x2 am = {0, 0};  // two u16 lanes of sign-cleared bf16 bits
 #pragma unroll
   for (int c = 0; c < NC; ++c) {
-    const int64_t k = static_cast<int64_t>(c) * 512 + lane * 8;
+    const int64_t k = static_cast<int64_t>(wave * NC + c) * 512 + lane * 8;
     if (k < K) {
       v[c] = *reinterpret_cast<const uint4*>(xr + k);
     } else {
@@ -130,17 +134,23 @@ __global__ __launch_bounds__(256) void quantize_rows_kernel(
   }
   uint32_t amax = am.x > am.y ? am.x : am.y;
   amax = wave_max_u32(amax);
+  if (nwaves > 1) {
+    if (lane == 0) wave_max[wave] = amax;
+    __syncthreads();
+    amax = wave_max[0];
+    for (int w = 1; w < nwaves; ++w) amax = amax > wave_max[w] ? amax : wave_max[w];
+  }
 
   // Non-negative floats order like their bit patterns, so the u16 max of the
   // sign-cleared bf16 bits is the bit pattern of the absolute maximum.
   const float a = __uint_as_float(amax << 16);
   const float s = a / 7.0f;
-  if (lane == 0) scale[row] = s;
+  if (threadIdx.x == 0) scale[row] = s;
 
   if (s == 0.0f) {
 #pragma unroll
     for (int c = 0; c < NC; ++c) {
-      const int64_t k = static_cast<int64_t>(c) * 512 + lane * 8;
+      const int64_t k = static_cast<int64_t>(wave * NC + c) * 512 + lane * 8;
       if (k < K) *reinterpret_cast<uint32_t*>(qr + k / 2) = 0u;
     }
     return;
@@ -150,7 +160,7 @@ __global__ __launch_bounds__(256) void quantize_rows_kernel(
   if (__builtin_isinf(rcp)) {
 #pragma unroll
     for (int c = 0; c < NC; ++c) {
-      const int64_t k = static_cast<int64_t>(c) * 512 + lane * 8;
+      const int64_t k = static_cast<int64_t>(wave * NC + c) * 512 + lane * 8;
       if (k < K) *reinterpret_cast<uint32_t*>(qr + k / 2) = pack8_exact(v[c], s);
     }
     return;
@@ -158,7 +168,7 @@ __global__ __launch_bounds__(256) void quantize_rows_kernel(
 
 #pragma unroll
   for (int c = 0; c < NC; ++c) {
-    const int64_t k = static_cast<int64_t>(c) * 512 + lane * 8;
+    const int64_t k = static_cast<int64_t>(wave * NC + c) * 512 + lane * 8;
     bool near = false;
     uint32_t p = pack8_fast(v[c], rcp, &near);
     if (near) p = pack8_exact(v[c], s);
@@ -207,9 +217,9 @@ __global__ __launch_bounds__(256) void quantize_rows_stream_kernel(
 }
 
 template <int NC>
-hipError_t launch_nc(const uint16_t* x, int64_t M, int64_t K, uint8_t* q, float* s, hipStream_t st) {
-  const dim3 grid(static_cast<unsigned>((M + 3) / 4));
-  hipLaunchKernelGGL(quantize_rows_kernel<NC>, grid, dim3(256), 0, st, x, M, K, q, s);
+hipError_t launch_nc(const uint16_t* x, int64_t M, int64_t K, uint8_t* q, float* s, int waves, hipStream_t st) {
+  hipLaunchKernelGGL(quantize_rows_kernel<NC>, dim3(static_cast<unsigned>(M)), dim3(64 * waves), 0, st, x, M, K,
+                     q, s);
   return hipGetLastError();
 }
 
@@ -217,16 +227,20 @@ hipError_t launch_nc(const uint16_t* x, int64_t M, int64_t K, uint8_t* q, float*
 
 hipError_t launch_quantize_rows(const uint16_t* x, int64_t M, int64_t K, uint8_t* q, float* s,
                                 hipStream_t st) {
-  const int64_t nc = (K + 511) / 512;
-  if (nc <= 1) return launch_nc<1>(x, M, K, q, s, st);
-  if (nc <= 2) return launch_nc<2>(x, M, K, q, s, st);
-  if (nc <= 4) return launch_nc<4>(x, M, K, q, s, st);
-  if (nc <= 6) return launch_nc<6>(x, M, K, q, s, st);
-  if (nc <= 8) return launch_nc<8>(x, M, K, q, s, st);
-  if (nc <= 12) return launch_nc<12>(x, M, K, q, s, st);
-  if (nc <= 16) return launch_nc<16>(x, M, K, q, s, st);
-  if (nc <= 24) return launch_nc<24>(x, M, K, q, s, st);
-  if (nc <= 32) return launch_nc<32>(x, M, K, q, s, st);
+  // A row of K elements is 'chunks' chunks of 512; it is split over up to 8
+  // waves of at most 4 chunks each, so that many small waves keep enough
+  // loads in flight and the last round of waves is short.
+  const int64_t chunks = (K + 511) / 512;
+  if (chunks <= 32) {
+    const int waves = static_cast<int>(chunks <= 4 ? 1 : (chunks + 3) / 4);
+    const int nc = static_cast<int>((chunks + waves - 1) / waves);
+    switch (nc) {
+      case 1: return launch_nc<1>(x, M, K, q, s, waves, st);
+      case 2: return launch_nc<2>(x, M, K, q, s, waves, st);
+      case 3: return launch_nc<3>(x, M, K, q, s, waves, st);
+      default: return launch_nc<4>(x, M, K, q, s, waves, st);
+    }
+  }
   const dim3 grid(static_cast<unsigned>((M + 3) / 4));
   hipLaunchKernelGGL(quantize_rows_stream_kernel, grid, dim3(256), 0, st, x, M, K, q, s);
   return hipGetLastError();
