@@ -177,9 +177,12 @@ __global__ __launch_bounds__(kThreads, 2) void w4a4_gemm_kernel(
     for (int j = 0; j < kWDma; ++j)
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rsw, (lds_void_t*)(buf + kXSlots + 64 * (kWDma * wave + j)), 16,
                                                ow[j] - back, kb, 0, 0);
+    // Same for the activation chunks past the row end: read an in-bounds
+    // chunk (never past the end of the operand), then zero the codes.
+    const uint32_t xback = (KTAIL && kb + 16 * xl_chunk >= row_bytes) ? 32u : 0u;
 #pragma unroll
     for (int i = 0; i < kXLoads; ++i)
-      gx[i] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rsx, ox[i], kb, 0));
+      gx[i] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rsx, ox[i] - xback, kb, 0));
     if (KTAIL && kb + 16 * xl_chunk >= row_bytes) {
 #pragma unroll
       for (int i = 0; i < kXLoads; ++i) gx[i] = make_uint4(0, 0, 0, 0);
