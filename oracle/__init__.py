@@ -22,3 +22,14 @@ from .w4a4 import (  # noqa: F401
     w4a4_linear,
     w4a4_linear_rows,
 )
+from .w158a4 import (  # noqa: F401
+    ternary_scale,
+    quantize_ternary,
+    pack_ternary,
+    unpack_ternary,
+    pack_weight_ternary,
+    w158a4_gemm,
+    w158a4_gemm_i32,
+    w158a4_linear,
+    w158a4_linear_rows,
+)
