@@ -146,6 +146,76 @@ jq_status jq_w4a4_gemm(const void* q_packed, const float* scale, int64_t M, int6
 jq_status jq_w4a4_gemm_i32(const void* q_packed, int64_t M, int64_t K,
                            const void* wq_packed, int64_t N, int32_t* acc, void* stream);
 
+/*
+ * ---------------------------------------------------------------------------
+ * W1.58A4: ternary weights with the same per-token int4 activations.
+ *
+ * Ternary (1.58-bit) weights with INT4 activations is the paper's W1.58A4
+ * deployment setting (Sec. 4 result tables, W1.58A4 rows; appendix
+ * experimental-details tables, "Ternary weights, INT4 activations"), run by
+ * the same plain operator: quantise, pack, low-bit GEMM, dequantise (Sec. 3.1,
+ * FAQ Q7).  The paper states no ternary formula; the library implements the
+ * absmean reading, one scale per output channel (row n of W [N,K]):
+ *
+ *     g[n]   = fl32(fl64(sum_k |w[n,k]|) / K)       (fp64 sum and division)
+ *     t[n,k] = clamp(rne(fl32(w[n,k] / g[n])), -1, 1),  t = 0 if g[n] = 0
+ *
+ * The fp64 sum is exact (so independent of summation order) when a row's
+ * nonzero magnitudes span less than 2^29.  The layer is the W4A4 layer with
+ * t and g in place of the int4 weight codes and scales:
+ *
+ *     acc[m,n] = sum_k qx[m,k] * t[n,k]                        (exact integer)
+ *     y[m,n]   = bf16_rne(((fl32(acc) * s_x[m]) * g[n]) + bias[n])
+ *
+ * Packed ternary layout: row-major [N, K/4] bytes; byte j of a row holds codes
+ * 4j .. 4j+3, code 4j+i in bits 2i .. 2i+1 as a 2-bit two's-complement field
+ * (0 -> 00, 1 -> 01, -1 -> 11).  Shapes, alignment and errors follow the
+ * conventions above; the packed weight operand (N*K/4 bytes) must stay below
+ * 2 GiB.
+ */
+
+/*
+ * Ternary weight quantisation and packing, once per layer at model load.
+ *   w_bf16    in   [N,K] bf16, 16-byte aligned
+ *   wt_packed out  [N,K/4] uint8 (packed ternary layout above), 16-byte aligned
+ *   w_scale   out  [N] fp32, g[n] as defined above
+ * Errors: JQ_ERR_INVALID_ARG, JQ_ERR_UNSUPPORTED_SHAPE, JQ_ERR_MISALIGNED, JQ_ERR_HIP.
+ */
+jq_status jq_pack_weight_ternary(const void* w_bf16, int64_t N, int64_t K,
+                                 void* wt_packed, float* w_scale, void* stream);
+
+/*
+ * The whole W1.58A4 linear: quantise x per token into the workspace (same
+ * size and layout as for jq_w4a4_linear, see jq_w4a4_workspace_bytes), then
+ * the int4 x ternary GEMM with the fused epilogue.
+ *   wt_packed, w_scale   in  [N,K/4] uint8 and [N] fp32 from jq_pack_weight_ternary
+ *   other arguments as jq_w4a4_linear
+ * Errors: as jq_w4a4_linear.
+ */
+jq_status jq_w158a4_linear(const void* x_bf16, int64_t M, int64_t K,
+                           const void* wt_packed, const float* w_scale, int64_t N,
+                           const void* bias_bf16, void* y_bf16,
+                           void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * GEMM + epilogue on already-quantised activations (from jq_quantize_act)
+ * and packed ternary weights.  Arguments as jq_w4a4_gemm with wt_packed
+ * [N,K/4] in place of wq_packed.
+ * Errors: JQ_ERR_INVALID_ARG, JQ_ERR_UNSUPPORTED_SHAPE, JQ_ERR_MISALIGNED, JQ_ERR_HIP.
+ */
+jq_status jq_w158a4_gemm(const void* q_packed, const float* scale, int64_t M, int64_t K,
+                         const void* wt_packed, const float* w_scale, int64_t N,
+                         const void* bias_bf16, void* y_bf16, void* stream);
+
+/*
+ * The exact integer contraction alone, for checking: acc[m,n] =
+ * sum_k qx[m,k] * t[n,k] as int32 [M,N] (16-byte aligned), by the same kernel
+ * as jq_w158a4_gemm with the epilogue replaced by a plain store.
+ * Errors: JQ_ERR_INVALID_ARG, JQ_ERR_UNSUPPORTED_SHAPE, JQ_ERR_MISALIGNED, JQ_ERR_HIP.
+ */
+jq_status jq_w158a4_gemm_i32(const void* q_packed, int64_t M, int64_t K,
+                             const void* wt_packed, int64_t N, int32_t* acc, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

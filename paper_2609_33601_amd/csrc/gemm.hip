@@ -70,12 +70,10 @@ constexpr int kBKB = 64;       // packed bytes of K per stage (128 codes)
 constexpr int kChunks = kBKB / 16;           // 16-byte packed chunks per row per stage
 constexpr int kXChunks = 2 * kChunks;        // 16-byte int8 chunks per activation row per stage
 constexpr int kXSlots = kBM * kXChunks;      // 16-byte slots of the int8 activation tile
-constexpr int kStageSlots = kXSlots + kBN * kChunks;
 constexpr int kThreads = 256;
 constexpr int kWM = 128, kWN = 64;           // per-wave tile: all activation rows, a quarter of the weight rows
 constexpr int kFM = kWM / 16, kFN = kWN / 16;
 constexpr int kXLoads = kBM * kChunks / kThreads;  // 16-byte activation loads per thread per stage
-constexpr int kWDma = kBN / 64;              // weight DMA instructions per wave per stage (16 rows each)
 constexpr int kGroupM = 8;
 constexpr int kNumXcd = 8;
 constexpr int kBufferFlags = 0x00020000;     // buffer descriptor word 3 for raw byte-addressed loads
@@ -84,9 +82,30 @@ constexpr int kWaitVm0 = (0x7 << 4) | (0xF << 8);  // s_waitcnt vmcnt(0), other 
 static_assert(kChunks == 4 && kXChunks == 8, "swizzles below assume 4 packed / 8 int8 chunks per LDS row");
 static_assert(kXLoads == 2, "activation staging below assumes two loads per thread");
 
+// Weight formats.  kInt4: codes -8..7, two per byte (the W4A4 layer).
+// kTernary: codes -1..1, four per byte as 2-bit fields (the W1.58A4 layer).
+// Per stage (128 codes of K) a weight row holds kWChunks 16-byte chunks; one
+// DMA instruction fills kDmaRows tile rows; kShift undoes the operand
+// scaling (activations enter the MFMA as 16 * code, int4 weights as 16 * code,
+// ternary weights as 64 * code).
+template <WeightFormat WF>
+struct WTraits {
+  static constexpr bool kTern = WF == WeightFormat::kTernary;
+  static constexpr int kWChunks = kTern ? 2 : 4;
+  static constexpr int kStageBytes = 16 * kWChunks;
+  static constexpr int kDmaRows = 64 / kWChunks;
+  static constexpr int kDma = kWN / kDmaRows;          // weight DMA instructions per wave per stage
+  static constexpr int kStageSlots = kXSlots + kBN * kWChunks;
+  static constexpr int kShift = kTern ? 10 : 8;
+  static constexpr int kUnpackValu = kTern ? 7 : 6;    // VALU instructions per widened weight fragment
+};
+
 // LDS slots (16-byte units): chunk c of packed weight row r, and int8 chunk c
 // of activation row r.
 __device__ __forceinline__ int w_slot(int row, int c) { return row * kChunks + (c ^ ((row >> 1) & 3)); }
+// Ternary weight rows are 32 bytes (two chunks); rows 8..15 of every 16 swap
+// their chunks, so the 32 lanes of a ds_read_b64 half cover all 64 banks.
+__device__ __forceinline__ int wt_slot(int row, int c) { return row * 2 + (c ^ ((row >> 3) & 1)); }
 __device__ __forceinline__ int x_slot(int row, int c) { return row * kXChunks + (c ^ (row & 7)); }
 
 __device__ __forceinline__ v4i unpack8(uint32_t p0, uint32_t p1) {
@@ -96,6 +115,37 @@ __device__ __forceinline__ v4i unpack8(uint32_t p0, uint32_t p1) {
   r[2] = static_cast<int>((p1 << 4) & 0xF0F0F0F0u);
   r[3] = static_cast<int>(p1 & 0xF0F0F0F0u);
   return r;
+}
+
+// Widen 16 ternary codes (one packed dword, code i in bits 2i .. 2i+1) to
+// int8 64 * code: dword d, byte b of the result holds code 4b + d.  Shifting
+// a 2-bit field to the top of its byte sign-extends it for free.
+__device__ __forceinline__ v4i unpack_tern(uint32_t p) {
+  v4i r;
+  r[0] = static_cast<int>((p << 6) & 0xC0C0C0C0u);
+  r[1] = static_cast<int>((p << 4) & 0xC0C0C0C0u);
+  r[2] = static_cast<int>((p << 2) & 0xC0C0C0C0u);
+  r[3] = static_cast<int>(p & 0xC0C0C0C0u);
+  return r;
+}
+
+// Widen 16 int4 activation codes (p0: codes 0..7, p1: codes 8..15) into the
+// order unpack_tern produces: dword d, byte b = 16 * code 4b + d.
+__device__ __forceinline__ v4i unpack8_tern_order(uint32_t p0, uint32_t p1) {
+  const v4i e = unpack8(p0, p1);  // e[0] = codes 0 2 4 6, e[1] = 1 3 5 7, e[2] = 8 10 12 14, e[3] = 9 11 13 15
+  v4i r;
+  // v_perm_b32: selector byte values 0..3 pick the second operand's bytes, 4..7 the first's.
+  r[0] = static_cast<int>(__builtin_amdgcn_perm(static_cast<uint32_t>(e[2]), static_cast<uint32_t>(e[0]), 0x06040200u));
+  r[1] = static_cast<int>(__builtin_amdgcn_perm(static_cast<uint32_t>(e[3]), static_cast<uint32_t>(e[1]), 0x06040200u));
+  r[2] = static_cast<int>(__builtin_amdgcn_perm(static_cast<uint32_t>(e[2]), static_cast<uint32_t>(e[0]), 0x07050301u));
+  r[3] = static_cast<int>(__builtin_amdgcn_perm(static_cast<uint32_t>(e[3]), static_cast<uint32_t>(e[1]), 0x07050301u));
+  return r;
+}
+
+// 16 bytes per lane from a buffer straight into LDS: lane i writes dst[i]
+// (buffer_load_dwordx4 ... lds, no registers involved).
+__device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t rs, uint4* dst, uint32_t voffset, int soffset) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void_t*)dst, 16, voffset, soffset, 0, 0);
 }
 
 struct TileCoord {
@@ -117,11 +167,13 @@ __device__ __forceinline__ bool tile_of_block(int bid, int tiles_m, int tiles_n,
   return true;
 }
 
-template <Epilogue EPI, bool HAS_BIAS, bool KTAIL>
+template <WeightFormat WF, Epilogue EPI, bool HAS_BIAS, bool KTAIL>
 __global__ __launch_bounds__(kThreads, 2) void w4a4_gemm_kernel(
     const uint8_t* __restrict__ qx, const float* __restrict__ sx, int M, int K,
     const uint8_t* __restrict__ qw, const float* __restrict__ sw, int N,
     const uint16_t* __restrict__ bias, void* __restrict__ out, int tiles_m, int tiles_n) {
+  using WT = WTraits<WF>;
+  constexpr int kStageSlots = WT::kStageSlots, kWDma = WT::kDma;
   // Two stage buffers, each the int8 activation tile followed by the packed weight tile.
   __shared__ uint4 lds[2 * kStageSlots];
 
@@ -136,7 +188,8 @@ __global__ __launch_bounds__(kThreads, 2) void w4a4_gemm_kernel(
   const int wn = wave;  // waves split the weight rows; each covers every activation row
   const int li = lane & 15, lg = lane >> 4;
 
-  const int64_t row_bytes = K / 2;
+  const int64_t row_bytes = K / 2;                       // packed activation row
+  const int64_t wrow_bytes = WT::kTern ? K / 4 : K / 2;  // packed weight row
   const int ksteps = static_cast<int>((row_bytes + kBKB - 1) / kBKB);
 
   // Buffer descriptors over the two packed operands (sizes < 2^31, checked by
@@ -144,17 +197,19 @@ __global__ __launch_bounds__(kThreads, 2) void w4a4_gemm_kernel(
   const __amdgpu_buffer_rsrc_t rsx =
       __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(qx), 0, static_cast<int>(M * row_bytes), kBufferFlags);
   const __amdgpu_buffer_rsrc_t rsw =
-      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(qw), 0, static_cast<int>(N * row_bytes), kBufferFlags);
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(qw), 0, static_cast<int>(N * wrow_bytes), kBufferFlags);
 
-  // Weight DMA: one instruction fills 16 tile rows R .. R + 15, i.e. LDS slots
-  // 4R .. 4R + 63 in lane order.  Lane l lands in slot 4R + l = row R + (l >> 2),
-  // swizzled chunk l & 3, so it fetches global chunk (l & 3) ^ ((l >> 3) & 3).
-  const int dma_chunk = (lane & 3) ^ ((lane >> 3) & 3);
+  // Weight DMA: one instruction fills kDmaRows tile rows R .. in lane order
+  // (int4: 16 rows of 4 slots, lane l -> row R + (l >> 2), swizzled chunk
+  // l & 3, so it fetches global chunk (l & 3) ^ ((l >> 3) & 3); ternary: 32
+  // rows of 2 slots, lane l -> row R + (l >> 1), global chunk
+  // (l & 1) ^ ((l >> 4) & 1)).
+  const int dma_chunk = WT::kTern ? ((lane & 1) ^ ((lane >> 4) & 1)) : ((lane & 3) ^ ((lane >> 3) & 3));
   uint32_t ow[kWDma];
 #pragma unroll
   for (int j = 0; j < kWDma; ++j) {
-    const int r = 16 * (kWDma * wave + j) + (lane >> 2);
-    ow[j] = static_cast<uint32_t>(min(n0 + r, N - 1)) * static_cast<uint32_t>(row_bytes) + 16 * dma_chunk;
+    const int r = WT::kDmaRows * (kWDma * wave + j) + (WT::kTern ? (lane >> 1) : (lane >> 2));
+    ow[j] = static_cast<uint32_t>(min(n0 + r, N - 1)) * static_cast<uint32_t>(wrow_bytes) + 16 * dma_chunk;
   }
   // Activation loads: thread loads packed chunk (tid & 3) of tile rows
   // (tid >> 2) + 64 i; it widens chunk c into int8 chunks 2c and 2c + 1.
@@ -169,14 +224,14 @@ __global__ __launch_bounds__(kThreads, 2) void w4a4_gemm_kernel(
   uint4 gx[kXLoads];
   auto issue = [&](uint4* buf, int ks) {
     const int kb = ks * kBKB;
-    // K % 128 == 64: in the last stage packed chunks 2 and 3 lie past the row
-    // end.  The weight DMA then fetches an in-bounds chunk instead; the
-    // activation codes there are zeroed, so those products vanish.
-    const uint32_t back = (KTAIL && kb + 16 * dma_chunk >= row_bytes) ? 32u : 0u;
+    const int kbw = ks * WT::kStageBytes;
+    // K % 128 == 64: in the last stage the upper half of every row (codes
+    // 64 .. 127) lies past the row end.  The weight DMA then fetches an
+    // in-bounds chunk instead; the activation codes there are zeroed, so
+    // those products vanish.
+    const uint32_t back = (KTAIL && kbw + 16 * dma_chunk >= wrow_bytes) ? WT::kStageBytes / 2 : 0u;
 #pragma unroll
-    for (int j = 0; j < kWDma; ++j)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsw, (lds_void_t*)(buf + kXSlots + 64 * (kWDma * wave + j)), 16,
-                                               ow[j] - back, kb, 0, 0);
+    for (int j = 0; j < kWDma; ++j) dma16(rsw, buf + kXSlots + 64 * (kWDma * wave + j), ow[j] - back, kbw);
     // Same for the activation chunks past the row end: read an in-bounds
     // chunk (never past the end of the operand), then zero the codes.
     const uint32_t xback = (KTAIL && kb + 16 * xl_chunk >= row_bytes) ? 32u : 0u;
@@ -192,8 +247,13 @@ __global__ __launch_bounds__(kThreads, 2) void w4a4_gemm_kernel(
 #pragma unroll
     for (int i = 0; i < kXLoads; ++i) {
       const int row = xl_row + 64 * i;
-      buf[x_slot(row, 2 * xl_chunk)] = __builtin_bit_cast(uint4, unpack8(gx[i].x, gx[i].y));
-      buf[x_slot(row, 2 * xl_chunk + 1)] = __builtin_bit_cast(uint4, unpack8(gx[i].z, gx[i].w));
+      if constexpr (WT::kTern) {
+        buf[x_slot(row, 2 * xl_chunk)] = __builtin_bit_cast(uint4, unpack8_tern_order(gx[i].x, gx[i].y));
+        buf[x_slot(row, 2 * xl_chunk + 1)] = __builtin_bit_cast(uint4, unpack8_tern_order(gx[i].z, gx[i].w));
+      } else {
+        buf[x_slot(row, 2 * xl_chunk)] = __builtin_bit_cast(uint4, unpack8(gx[i].x, gx[i].y));
+        buf[x_slot(row, 2 * xl_chunk + 1)] = __builtin_bit_cast(uint4, unpack8(gx[i].z, gx[i].w));
+      }
     }
   };
 
@@ -207,10 +267,20 @@ __global__ __launch_bounds__(kThreads, 2) void w4a4_gemm_kernel(
   // into `nxt`, run both MFMA half-stages, wait, write the widened activation
   // tile of stage ks + 1, barrier.
   auto stage = [&](const uint4* cur, uint4* nxt, int ks) {
+    // Lane group lg covers codes 32 lg .. 32 lg + 31 of the stage: 16 packed
+    // bytes of an int4 row, 8 of a ternary row.
     uint4 pw[kFN];
-    v4i bx0[kFM], bx1[kFM];
 #pragma unroll
-    for (int f = 0; f < kFN; ++f) pw[f] = cur[kXSlots + w_slot(kWN * wn + 16 * f + li, lg)];
+    for (int f = 0; f < kFN; ++f) {
+      const int row = kWN * wn + 16 * f + li;
+      if constexpr (WT::kTern) {
+        const uint2 v = reinterpret_cast<const uint2*>(cur + kXSlots)[2 * wt_slot(row, lg >> 1) + (lg & 1)];
+        pw[f] = make_uint4(v.x, v.y, 0, 0);
+      } else {
+        pw[f] = cur[kXSlots + w_slot(row, lg)];
+      }
+    }
+    v4i bx0[kFM], bx1[kFM];
 #pragma unroll
     for (int f = 0; f < kFM; ++f) bx0[f] = __builtin_bit_cast(v4i, cur[x_slot(16 * f + li, 2 * lg)]);
 #pragma unroll
@@ -220,7 +290,7 @@ __global__ __launch_bounds__(kThreads, 2) void w4a4_gemm_kernel(
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int fn = 0; fn < kFN; ++fn) {
-      const v4i aw = unpack8(pw[fn].x, pw[fn].y);
+      const v4i aw = WT::kTern ? unpack_tern(pw[fn].x) : unpack8(pw[fn].x, pw[fn].y);
 #pragma unroll
       for (int fm = 0; fm < kFM; ++fm)
         acc[fn][fm] = __builtin_amdgcn_mfma_i32_16x16x64_i8(aw, bx0[fm], acc[fn][fm], 0, 0, 0);
@@ -228,13 +298,13 @@ __global__ __launch_bounds__(kThreads, 2) void w4a4_gemm_kernel(
     // Widen each weight fragment just before its row of MFMAs.
 #pragma unroll
     for (int fn = 0; fn < kFN; ++fn) {
-      __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);
+      __builtin_amdgcn_sched_group_barrier(0x002, WT::kUnpackValu, 0);
       __builtin_amdgcn_sched_group_barrier(0x008, kFM, 0);
     }
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int fn = 0; fn < kFN; ++fn) {
-      const v4i aw = unpack8(pw[fn].z, pw[fn].w);
+      const v4i aw = WT::kTern ? unpack_tern(pw[fn].y) : unpack8(pw[fn].z, pw[fn].w);
 #pragma unroll
       for (int fm = 0; fm < kFM; ++fm)
         acc[fn][fm] = __builtin_amdgcn_mfma_i32_16x16x64_i8(aw, bx1[fm], acc[fn][fm], 0, 0, 0);
@@ -242,7 +312,7 @@ __global__ __launch_bounds__(kThreads, 2) void w4a4_gemm_kernel(
     // Widen each weight fragment just before its four MFMAs.
 #pragma unroll
     for (int fn = 0; fn < kFN; ++fn) {
-      __builtin_amdgcn_sched_group_barrier(0x002, 6, 1);
+      __builtin_amdgcn_sched_group_barrier(0x002, WT::kUnpackValu, 1);
       __builtin_amdgcn_sched_group_barrier(0x008, 4, 1);
     }
     __builtin_amdgcn_sched_barrier(0);
@@ -275,7 +345,7 @@ __global__ __launch_bounds__(kThreads, 2) void w4a4_gemm_kernel(
       for (int fm = 0; fm < kFM; ++fm) {
         const int m = mb + 16 * fm;
         const v4i a = acc[fn][fm];
-        const int v0 = a[0] >> 8, v1 = a[1] >> 8, v2 = a[2] >> 8, v3 = a[3] >> 8;
+        const int v0 = a[0] >> WT::kShift, v1 = a[1] >> WT::kShift, v2 = a[2] >> WT::kShift, v3 = a[3] >> WT::kShift;
         int32_t* p = o + static_cast<int64_t>(m) * N + n;
         if (full) {
           *reinterpret_cast<int4*>(p) = make_int4(v0, v1, v2, v3);
@@ -309,7 +379,7 @@ __global__ __launch_bounds__(kThreads, 2) void w4a4_gemm_kernel(
         uint16_t h[4];
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          float f = static_cast<float>(a[r] >> 8);
+          float f = static_cast<float>(a[r] >> WT::kShift);
           f = f * sxv[fm];
           f = f * swv[r];
           if (HAS_BIAS) f = f + bv[r];
@@ -333,7 +403,7 @@ __global__ __launch_bounds__(kThreads, 2) void w4a4_gemm_kernel(
 
 hipError_t launch_w4a4_gemm(Epilogue epi, const uint8_t* qx, const float* sx, int64_t M, int64_t K,
                             const uint8_t* qw, const float* sw, int64_t N, const uint16_t* bias,
-                            void* out, hipStream_t st) {
+                            void* out, hipStream_t st, WeightFormat wf) {
   const int tiles_m = static_cast<int>((M + kBM - 1) / kBM);
   const int tiles_n = static_cast<int>((N + kBN - 1) / kBN);
   const int64_t T = static_cast<int64_t>(tiles_m) * tiles_n;
@@ -342,16 +412,26 @@ hipError_t launch_w4a4_gemm(Epilogue epi, const uint8_t* qx, const float* sx, in
   const dim3 block(kThreads);
   const int Mi = static_cast<int>(M), Ki = static_cast<int>(K), Ni = static_cast<int>(N);
   const bool tail = (K % 128) != 0;
-#define JQ_LAUNCH(E, B, T)                                                                      \
-  hipLaunchKernelGGL((w4a4_gemm_kernel<E, B, T>), grid, block, 0, st, qx, sx, Mi, Ki, qw, sw, Ni, \
+#define JQ_LAUNCH(W, E, B, T)                                                                      \
+  hipLaunchKernelGGL((w4a4_gemm_kernel<W, E, B, T>), grid, block, 0, st, qx, sx, Mi, Ki, qw, sw, Ni, \
                      bias, out, tiles_m, tiles_n)
-  if (epi == Epilogue::kInt32) {
-    if (tail) JQ_LAUNCH(Epilogue::kInt32, false, true); else JQ_LAUNCH(Epilogue::kInt32, false, false);
-  } else if (bias != nullptr) {
-    if (tail) JQ_LAUNCH(Epilogue::kBf16, true, true); else JQ_LAUNCH(Epilogue::kBf16, true, false);
-  } else {
-    if (tail) JQ_LAUNCH(Epilogue::kBf16, false, true); else JQ_LAUNCH(Epilogue::kBf16, false, false);
+#define JQ_DISPATCH(W)                                                                    \
+  if (epi == Epilogue::kInt32) {                                                          \
+    if (tail) JQ_LAUNCH(W, Epilogue::kInt32, false, true);                                \
+    else JQ_LAUNCH(W, Epilogue::kInt32, false, false);                                    \
+  } else if (bias != nullptr) {                                                           \
+    if (tail) JQ_LAUNCH(W, Epilogue::kBf16, true, true);                                  \
+    else JQ_LAUNCH(W, Epilogue::kBf16, true, false);                                      \
+  } else {                                                                                \
+    if (tail) JQ_LAUNCH(W, Epilogue::kBf16, false, true);                                 \
+    else JQ_LAUNCH(W, Epilogue::kBf16, false, false);                                     \
   }
+  if (wf == WeightFormat::kTernary) {
+    JQ_DISPATCH(WeightFormat::kTernary)
+  } else {
+    JQ_DISPATCH(WeightFormat::kInt4)
+  }
+#undef JQ_DISPATCH
 #undef JQ_LAUNCH
   return hipGetLastError();
 }

@@ -37,7 +37,8 @@ jq_status quantize_common(const void* x, int64_t rows, int64_t K, void* q, float
 }
 
 jq_status check_gemm(const void* qx, const float* sx, int64_t M, int64_t K, const void* qw,
-                     const float* sw, int64_t N, const void* bias, const void* y, bool need_scales) {
+                     const float* sw, int64_t N, const void* bias, const void* y, bool need_scales,
+                     jq::WeightFormat wf = jq::WeightFormat::kInt4) {
   if (qx == nullptr || qw == nullptr || y == nullptr) return JQ_ERR_INVALID_ARG;
   if (need_scales && (sx == nullptr || sw == nullptr)) return JQ_ERR_INVALID_ARG;
   jq_status st = check_shape(M, K);
@@ -47,11 +48,57 @@ jq_status check_gemm(const void* qx, const float* sx, int64_t M, int64_t K, cons
   // The tile grid is indexed with 32-bit integers, and each packed operand is
   // addressed through a buffer descriptor with a 31-bit size.
   if (((M + 255) / 256) * ((N + 255) / 256) > (int64_t(1) << 26)) return JQ_ERR_UNSUPPORTED_SHAPE;
-  if (M * (K / 2) >= (int64_t(1) << 31) || N * (K / 2) >= (int64_t(1) << 31)) return JQ_ERR_UNSUPPORTED_SHAPE;
+  const int64_t wrow = wf == jq::WeightFormat::kTernary ? K / 4 : K / 2;
+  if (M * (K / 2) >= (int64_t(1) << 31) || N * wrow >= (int64_t(1) << 31)) return JQ_ERR_UNSUPPORTED_SHAPE;
   if (!aligned(qx, 16) || !aligned(qw, 16) || !aligned(y, 16)) return JQ_ERR_MISALIGNED;
   if ((sx != nullptr && !aligned(sx, 4)) || (sw != nullptr && !aligned(sw, 4))) return JQ_ERR_MISALIGNED;
   if (bias != nullptr && !aligned(bias, 2)) return JQ_ERR_MISALIGNED;
   return JQ_OK;
+}
+
+size_t workspace_bytes(int64_t M, int64_t K) {
+  if (check_shape(M, K) != JQ_OK) return 0;
+  return round_up(static_cast<size_t>(M) * static_cast<size_t>(K / 2), kWsAlign) +
+         round_up(static_cast<size_t>(M) * sizeof(float), kWsAlign);
+}
+
+// Quantise x into the workspace, then the GEMM with the fused epilogue.
+jq_status linear_common(const void* x_bf16, int64_t M, int64_t K, const void* w_packed, const float* w_scale,
+                        int64_t N, const void* bias_bf16, void* y_bf16, void* workspace, size_t ws_bytes,
+                        void* stream, jq::WeightFormat wf) {
+  if (x_bf16 == nullptr || workspace == nullptr) return JQ_ERR_INVALID_ARG;
+  jq_status st = check_gemm(x_bf16, w_scale, M, K, w_packed, w_scale, N, bias_bf16, y_bf16, true, wf);
+  if (st != JQ_OK) return st;
+  if (!aligned(workspace, kWsAlign)) return JQ_ERR_MISALIGNED;
+  if (ws_bytes < workspace_bytes(M, K)) return JQ_ERR_WORKSPACE_TOO_SMALL;
+
+  uint8_t* qx = static_cast<uint8_t*>(workspace);
+  float* sx = reinterpret_cast<float*>(qx + round_up(static_cast<size_t>(M) * static_cast<size_t>(K / 2), kWsAlign));
+  hipError_t e = jq::launch_quantize_rows(static_cast<const uint16_t*>(x_bf16), M, K, qx, sx,
+                                          as_stream(stream));
+  if (e != hipSuccess) return JQ_ERR_HIP;
+  e = jq::launch_w4a4_gemm(jq::Epilogue::kBf16, qx, sx, M, K, static_cast<const uint8_t*>(w_packed), w_scale, N,
+                           static_cast<const uint16_t*>(bias_bf16), y_bf16, as_stream(stream), wf);
+  return from_hip(e);
+}
+
+jq_status gemm_common(const void* q_packed, const float* scale, int64_t M, int64_t K, const void* w_packed,
+                      const float* w_scale, int64_t N, const void* bias_bf16, void* y_bf16, void* stream,
+                      jq::WeightFormat wf) {
+  const jq_status st = check_gemm(q_packed, scale, M, K, w_packed, w_scale, N, bias_bf16, y_bf16, true, wf);
+  if (st != JQ_OK) return st;
+  return from_hip(jq::launch_w4a4_gemm(jq::Epilogue::kBf16, static_cast<const uint8_t*>(q_packed), scale, M, K,
+                                       static_cast<const uint8_t*>(w_packed), w_scale, N,
+                                       static_cast<const uint16_t*>(bias_bf16), y_bf16, as_stream(stream), wf));
+}
+
+jq_status gemm_i32_common(const void* q_packed, int64_t M, int64_t K, const void* w_packed, int64_t N,
+                          int32_t* acc, void* stream, jq::WeightFormat wf) {
+  const jq_status st = check_gemm(q_packed, nullptr, M, K, w_packed, nullptr, N, nullptr, acc, false, wf);
+  if (st != JQ_OK) return st;
+  return from_hip(jq::launch_w4a4_gemm(jq::Epilogue::kInt32, static_cast<const uint8_t*>(q_packed), nullptr, M,
+                                       K, static_cast<const uint8_t*>(w_packed), nullptr, N, nullptr, acc,
+                                       as_stream(stream), wf));
 }
 
 }  // namespace
@@ -82,48 +129,54 @@ jq_status jq_pack_weight_int4(const void* w_bf16, int64_t N, int64_t K, void* wq
   return quantize_common(w_bf16, N, K, wq_packed, w_scale, stream);
 }
 
-size_t jq_w4a4_workspace_bytes(int64_t M, int64_t K) {
-  if (check_shape(M, K) != JQ_OK) return 0;
-  return round_up(static_cast<size_t>(M) * static_cast<size_t>(K / 2), kWsAlign) +
-         round_up(static_cast<size_t>(M) * sizeof(float), kWsAlign);
-}
+size_t jq_w4a4_workspace_bytes(int64_t M, int64_t K) { return workspace_bytes(M, K); }
 
 jq_status jq_w4a4_linear(const void* x_bf16, int64_t M, int64_t K, const void* wq_packed,
                          const float* w_scale, int64_t N, const void* bias_bf16, void* y_bf16,
                          void* workspace, size_t workspace_bytes, void* stream) {
-  if (x_bf16 == nullptr || workspace == nullptr) return JQ_ERR_INVALID_ARG;
-  jq_status st = check_gemm(x_bf16, w_scale, M, K, wq_packed, w_scale, N, bias_bf16, y_bf16, true);
-  if (st != JQ_OK) return st;
-  if (!aligned(workspace, kWsAlign)) return JQ_ERR_MISALIGNED;
-  if (workspace_bytes < jq_w4a4_workspace_bytes(M, K)) return JQ_ERR_WORKSPACE_TOO_SMALL;
-
-  uint8_t* qx = static_cast<uint8_t*>(workspace);
-  float* sx = reinterpret_cast<float*>(qx + round_up(static_cast<size_t>(M) * static_cast<size_t>(K / 2), kWsAlign));
-  hipError_t e = jq::launch_quantize_rows(static_cast<const uint16_t*>(x_bf16), M, K, qx, sx,
-                                          as_stream(stream));
-  if (e != hipSuccess) return JQ_ERR_HIP;
-  e = jq::launch_w4a4_gemm(jq::Epilogue::kBf16, qx, sx, M, K, static_cast<const uint8_t*>(wq_packed),
-                           w_scale, N, static_cast<const uint16_t*>(bias_bf16), y_bf16, as_stream(stream));
-  return from_hip(e);
+  return linear_common(x_bf16, M, K, wq_packed, w_scale, N, bias_bf16, y_bf16, workspace, workspace_bytes, stream,
+                       jq::WeightFormat::kInt4);
 }
 
 jq_status jq_w4a4_gemm(const void* q_packed, const float* scale, int64_t M, int64_t K,
                        const void* wq_packed, const float* w_scale, int64_t N, const void* bias_bf16,
                        void* y_bf16, void* stream) {
-  const jq_status st = check_gemm(q_packed, scale, M, K, wq_packed, w_scale, N, bias_bf16, y_bf16, true);
-  if (st != JQ_OK) return st;
-  return from_hip(jq::launch_w4a4_gemm(jq::Epilogue::kBf16, static_cast<const uint8_t*>(q_packed), scale,
-                                       M, K, static_cast<const uint8_t*>(wq_packed), w_scale, N,
-                                       static_cast<const uint16_t*>(bias_bf16), y_bf16, as_stream(stream)));
+  return gemm_common(q_packed, scale, M, K, wq_packed, w_scale, N, bias_bf16, y_bf16, stream,
+                     jq::WeightFormat::kInt4);
 }
 
 jq_status jq_w4a4_gemm_i32(const void* q_packed, int64_t M, int64_t K, const void* wq_packed, int64_t N,
                            int32_t* acc, void* stream) {
-  const jq_status st = check_gemm(q_packed, nullptr, M, K, wq_packed, nullptr, N, nullptr, acc, false);
+  return gemm_i32_common(q_packed, M, K, wq_packed, N, acc, stream, jq::WeightFormat::kInt4);
+}
+
+jq_status jq_pack_weight_ternary(const void* w_bf16, int64_t N, int64_t K, void* wt_packed, float* w_scale,
+                                 void* stream) {
+  if (w_bf16 == nullptr || wt_packed == nullptr || w_scale == nullptr) return JQ_ERR_INVALID_ARG;
+  const jq_status st = check_shape(N, K);
   if (st != JQ_OK) return st;
-  return from_hip(jq::launch_w4a4_gemm(jq::Epilogue::kInt32, static_cast<const uint8_t*>(q_packed),
-                                       nullptr, M, K, static_cast<const uint8_t*>(wq_packed), nullptr, N,
-                                       nullptr, acc, as_stream(stream)));
+  if (!aligned(w_bf16, 16) || !aligned(wt_packed, 16) || !aligned(w_scale, 4)) return JQ_ERR_MISALIGNED;
+  return from_hip(jq::launch_ternary_rows(static_cast<const uint16_t*>(w_bf16), N, K,
+                                          static_cast<uint8_t*>(wt_packed), w_scale, as_stream(stream)));
+}
+
+jq_status jq_w158a4_linear(const void* x_bf16, int64_t M, int64_t K, const void* wt_packed,
+                           const float* w_scale, int64_t N, const void* bias_bf16, void* y_bf16,
+                           void* workspace, size_t workspace_bytes, void* stream) {
+  return linear_common(x_bf16, M, K, wt_packed, w_scale, N, bias_bf16, y_bf16, workspace, workspace_bytes, stream,
+                       jq::WeightFormat::kTernary);
+}
+
+jq_status jq_w158a4_gemm(const void* q_packed, const float* scale, int64_t M, int64_t K,
+                         const void* wt_packed, const float* w_scale, int64_t N, const void* bias_bf16,
+                         void* y_bf16, void* stream) {
+  return gemm_common(q_packed, scale, M, K, wt_packed, w_scale, N, bias_bf16, y_bf16, stream,
+                     jq::WeightFormat::kTernary);
+}
+
+jq_status jq_w158a4_gemm_i32(const void* q_packed, int64_t M, int64_t K, const void* wt_packed, int64_t N,
+                             int32_t* acc, void* stream) {
+  return gemm_i32_common(q_packed, M, K, wt_packed, N, acc, stream, jq::WeightFormat::kTernary);
 }
 
 }  // extern "C"

@@ -19,14 +19,20 @@ constexpr int64_t kMaxRows = int64_t(1) << 30;
 hipError_t launch_quantize_rows(const uint16_t* x, int64_t M, int64_t K, uint8_t* q, float* scale,
                                 hipStream_t st);
 
+// Ternary weight quantiser: w [N,K] bf16 -> t [N,K/4] 2-bit codes, g [N] fp32.
+hipError_t launch_ternary_rows(const uint16_t* w, int64_t N, int64_t K, uint8_t* t, float* g, hipStream_t st);
+
 enum class Epilogue { kBf16, kInt32 };
 
-// Packed int4 GEMM: acc[m,n] = sum_k qx[m,k] * qw[n,k] followed by the epilogue.
+// Weight operand of the GEMM: packed int4 [N,K/2] or packed ternary [N,K/4].
+enum class WeightFormat { kInt4, kTernary };
+
+// Packed low-bit GEMM: acc[m,n] = sum_k qx[m,k] * qw[n,k] followed by the epilogue.
 //   kBf16:  y[m,n] = bf16(((fp32(acc) * sx[m]) * sw[n]) + bias[n])  (bias may be null)
 //   kInt32: out[m,n] = acc
 hipError_t launch_w4a4_gemm(Epilogue epi, const uint8_t* qx, const float* sx, int64_t M, int64_t K,
                             const uint8_t* qw, const float* sw, int64_t N, const uint16_t* bias,
-                            void* out, hipStream_t st);
+                            void* out, hipStream_t st, WeightFormat wf = WeightFormat::kInt4);
 
 }  // namespace jq
 

@@ -30,6 +30,10 @@ SIGNATURES = {
     "jq_w4a4_linear": (ctypes.c_int, [_vp, _i64, _i64, _vp, _fp, _i64, _vp, _vp, _vp, _sz, _vp]),
     "jq_w4a4_gemm": (ctypes.c_int, [_vp, _fp, _i64, _i64, _vp, _fp, _i64, _vp, _vp, _vp]),
     "jq_w4a4_gemm_i32": (ctypes.c_int, [_vp, _i64, _i64, _vp, _i64, _ip, _vp]),
+    "jq_pack_weight_ternary": (ctypes.c_int, [_vp, _i64, _i64, _vp, _fp, _vp]),
+    "jq_w158a4_linear": (ctypes.c_int, [_vp, _i64, _i64, _vp, _fp, _i64, _vp, _vp, _vp, _sz, _vp]),
+    "jq_w158a4_gemm": (ctypes.c_int, [_vp, _fp, _i64, _i64, _vp, _fp, _i64, _vp, _vp, _vp]),
+    "jq_w158a4_gemm_i32": (ctypes.c_int, [_vp, _i64, _i64, _vp, _i64, _ip, _vp]),
 }
 
 _lib = None
@@ -181,6 +185,79 @@ def jq_w4a4_gemm_i32(q, wq, acc=None, stream=None):
                                 _dev(wq, torch.uint8, (N, Kh), "wq"), N,
                                 _dev(acc, torch.int32, (M, N), "acc"), _stream_ptr(stream))
     _check(st, "jq_w4a4_gemm_i32")
+    return acc
+
+
+# ---------------------------------------------------------------------------
+# W1.58A4: ternary weights [N, K/4], same activation path
+# ---------------------------------------------------------------------------
+
+
+def jq_pack_weight_ternary(w, wt=None, w_scale=None, stream=None):
+    """w bf16 [N,K] -> (wt uint8 [N,K/4] packed ternary codes, w_scale fp32 [N])."""
+    torch = _torch()
+    N, K = w.shape
+    if wt is None:
+        wt = torch.empty((N, K // 4), dtype=torch.uint8, device=w.device)
+    if w_scale is None:
+        w_scale = torch.empty((N,), dtype=torch.float32, device=w.device)
+    st = lib().jq_pack_weight_ternary(_dev(w, torch.bfloat16, None, "w"), N, K,
+                                      _dev(wt, torch.uint8, (N, K // 4), "wt"),
+                                      _dev(w_scale, torch.float32, (N,), "w_scale"), _stream_ptr(stream))
+    _check(st, "jq_pack_weight_ternary")
+    return wt, w_scale
+
+
+def jq_w158a4_linear(x, wt, w_scale, bias=None, y=None, workspace=None, stream=None):
+    """y = W1.58A4 linear of x (bf16 [M,K]) with a packed ternary weight; returns bf16 [M,N]."""
+    torch = _torch()
+    M, K = x.shape
+    N = wt.shape[0]
+    if y is None:
+        y = torch.empty((M, N), dtype=torch.bfloat16, device=x.device)
+    need = jq_w4a4_workspace_bytes(M, K)
+    if workspace is None:
+        workspace = torch.empty((need,), dtype=torch.uint8, device=x.device)
+    bptr = ctypes.c_void_p(None) if bias is None else _dev(bias, torch.bfloat16, (N,), "bias")
+    st = lib().jq_w158a4_linear(_dev(x, torch.bfloat16, None, "x"), M, K,
+                                _dev(wt, torch.uint8, (N, K // 4), "wt"),
+                                _dev(w_scale, torch.float32, (N,), "w_scale"), N, bptr,
+                                _dev(y, torch.bfloat16, (M, N), "y"),
+                                _dev(workspace, torch.uint8, None, "workspace"),
+                                workspace.numel(), _stream_ptr(stream))
+    _check(st, "jq_w158a4_linear")
+    return y
+
+
+def jq_w158a4_gemm(q, scale, wt, w_scale, bias=None, y=None, stream=None):
+    """GEMM + epilogue of pre-quantised activations with ternary weights; returns bf16 [M,N]."""
+    torch = _torch()
+    M, Kh = q.shape
+    K = 2 * Kh
+    N = wt.shape[0]
+    if y is None:
+        y = torch.empty((M, N), dtype=torch.bfloat16, device=q.device)
+    bptr = ctypes.c_void_p(None) if bias is None else _dev(bias, torch.bfloat16, (N,), "bias")
+    st = lib().jq_w158a4_gemm(_dev(q, torch.uint8, (M, Kh), "q"), _dev(scale, torch.float32, (M,), "scale"),
+                              M, K, _dev(wt, torch.uint8, (N, K // 4), "wt"),
+                              _dev(w_scale, torch.float32, (N,), "w_scale"), N, bptr,
+                              _dev(y, torch.bfloat16, (M, N), "y"), _stream_ptr(stream))
+    _check(st, "jq_w158a4_gemm")
+    return y
+
+
+def jq_w158a4_gemm_i32(q, wt, acc=None, stream=None):
+    """Exact accumulators int32 [M,N] of int4 activation codes times ternary weight codes."""
+    torch = _torch()
+    M, Kh = q.shape
+    K = 2 * Kh
+    N = wt.shape[0]
+    if acc is None:
+        acc = torch.empty((M, N), dtype=torch.int32, device=q.device)
+    st = lib().jq_w158a4_gemm_i32(_dev(q, torch.uint8, (M, Kh), "q"), M, K,
+                                  _dev(wt, torch.uint8, (N, K // 4), "wt"), N,
+                                  _dev(acc, torch.int32, (M, N), "acc"), _stream_ptr(stream))
+    _check(st, "jq_w158a4_gemm_i32")
     return acc
 
 

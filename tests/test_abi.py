@@ -31,7 +31,7 @@ def header_functions():
 
 def test_exports_every_declared_symbol():
     names = header_functions()
-    assert len(names) == 8, names
+    assert len(names) == 12, names
     lib = ctypes.CDLL(jq.LIB_PATH)
     for n in names:
         assert hasattr(lib, n), f"libjq.so does not export {n}"
@@ -54,7 +54,7 @@ def test_workspace_bytes():
     assert L.jq_w4a4_workspace_bytes(8, 100) == 0
 
 
-@pytest.mark.parametrize("fn", ["jq_quantize_act", "jq_pack_weight_int4"])
+@pytest.mark.parametrize("fn", ["jq_quantize_act", "jq_pack_weight_int4", "jq_pack_weight_ternary"])
 def test_quantize_validation(fn):
     f = getattr(jq.lib(), fn)
     assert f(None, 8, 64, A, A, None) == jq.JQ_ERR_INVALID_ARG
@@ -71,8 +71,9 @@ def test_quantize_validation(fn):
     assert f(A, 8, 64, A, A + 1, None) == jq.JQ_ERR_MISALIGNED
 
 
-def test_linear_validation():
-    f = jq.lib().jq_w4a4_linear
+@pytest.mark.parametrize("fn", ["jq_w4a4_linear", "jq_w158a4_linear"])
+def test_linear_validation(fn):
+    f = getattr(jq.lib(), fn)
     need = jq.lib().jq_w4a4_workspace_bytes(16, 128)
     ok = dict(x=A, M=16, K=128, wq=A, sw=A, N=32, b=None, y=A, ws=A, wsb=need, s=None)
 
@@ -96,15 +97,16 @@ def test_linear_validation():
     assert call(wsb=0) == jq.JQ_ERR_WORKSPACE_TOO_SMALL
 
 
-def test_gemm_validation():
-    g = jq.lib().jq_w4a4_gemm
+@pytest.mark.parametrize("fmt", ["w4a4", "w158a4"])
+def test_gemm_validation(fmt):
+    g = getattr(jq.lib(), f"jq_{fmt}_gemm")
     assert g(None, A, 4, 64, A, A, 4, None, A, None) == jq.JQ_ERR_INVALID_ARG
     assert g(A, None, 4, 64, A, A, 4, None, A, None) == jq.JQ_ERR_INVALID_ARG
     assert g(A, A, 4, 64, A, None, 4, None, A, None) == jq.JQ_ERR_INVALID_ARG
     assert g(A, A, 4, 64, A, A, 4, None, None, None) == jq.JQ_ERR_INVALID_ARG
     assert g(A, A, 4, 192 + 32, A, A, 4, None, A, None) == jq.JQ_ERR_UNSUPPORTED_SHAPE
     assert g(A + 8, A, 4, 64, A, A, 4, None, A, None) == jq.JQ_ERR_MISALIGNED
-    i = jq.lib().jq_w4a4_gemm_i32
+    i = getattr(jq.lib(), f"jq_{fmt}_gemm_i32")
     assert i(None, 4, 64, A, 4, A, None) == jq.JQ_ERR_INVALID_ARG
     assert i(A, 4, 64, A, 4, None, None) == jq.JQ_ERR_INVALID_ARG
     assert i(A, 4, 64, A, -1, A, None) == jq.JQ_ERR_INVALID_ARG
@@ -112,6 +114,9 @@ def test_gemm_validation():
     assert i(A, 4, 64, A, 4, A + 4, None) == jq.JQ_ERR_MISALIGNED
     assert i(A, 1 << 30, 64, A, 1 << 20, A, None) == jq.JQ_ERR_UNSUPPORTED_SHAPE
     assert i(A, 1 << 20, 4096, A, 64, A, None) == jq.JQ_ERR_UNSUPPORTED_SHAPE  # 2 GiB packed activations
+    # 2 GiB packed weights: N*K/2 bytes for int4, N*K/4 for ternary
+    big_n = (1 << 16) if fmt == "w4a4" else (1 << 17)
+    assert i(A, 64, 65536, A, big_n, A, None) == jq.JQ_ERR_UNSUPPORTED_SHAPE
 
 
 def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
