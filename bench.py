@@ -12,7 +12,12 @@ seeded synthetic tensors already resident in HBM.
 value = sum(2 M N K) / step time, in TOPS.  The line also carries the roofline
 of the dominant kernel (the down-projection GEMM), timed per launch with HIP
 events on the stream the library launches on, and the CPU oracle timed on a
-bounded sample of the same rows on the host cores.
+the whole step on the host cores (repeated until about ten seconds have passed).
+
+`secondary` reports, from the same run, the same measurement for other
+layers: the FLUX MLP step with ternary weights (W1.58A4), the 8B
+diffusion-LLM block linears (W4A4 and W1.58A4) and the DiT attention
+projection and fused QKV linears.
 """
 
 import argparse
@@ -35,7 +40,8 @@ def parse_args():
     p.add_argument("--steps", type=int, default=200)
     p.add_argument("--warmup", type=int, default=20)
     p.add_argument("--no-cpu-baseline", action="store_true", help="skip the oracle CPU baseline leg")
-    p.add_argument("--cpu-seconds", type=float, default=12.0, help="target CPU time of the oracle sample")
+    p.add_argument("--cpu-seconds", type=float, default=10.0, help="minimum CPU time of the oracle baseline")
+    p.add_argument("--no-secondary", action="store_true", help="skip the secondary workloads")
     p.add_argument("--copy-calib", action="store_true",
                    help="also run a plain 256 MiB device copy (calibrates HBM byte counters under rocprofv3)")
     return p.parse_args()
@@ -67,17 +73,33 @@ def log(*a):
     print("[bench]", *a, file=sys.stderr, flush=True)
 
 
-class Prepared:
-    """Device-resident inputs, packed weight and output/workspace buffers of one linear."""
+_X_CACHE = {}
 
-    def __init__(self, lin, torch, jq):
+
+def _make_x(lin):
+    key = (lin.M, lin.K, lin.x_dist, lin.x_seed, lin.outlier_frac, lin.outlier_factor)
+    if key not in _X_CACHE:
+        _X_CACHE[key] = lin.make_x()
+    return _X_CACHE[key]
+
+
+class Prepared:
+    """Device-resident inputs, packed weight and output/workspace buffers of one linear.
+
+    fmt "int4" packs the weight for the W4A4 layer, "ternary" for W1.58A4.
+    """
+
+    def __init__(self, lin, torch, jq, fmt="int4"):
         self.lin = lin
-        self.x_bits = lin.make_x()
+        self.fmt = fmt
+        self.x_bits = _make_x(lin)
         self.w_bits = lin.make_w()
         self.b_bits = lin.make_bias()
         self.x = jq.bf16_tensor(self.x_bits, "cuda")
         w = jq.bf16_tensor(self.w_bits, "cuda")
-        self.wq, self.sw = jq.jq_pack_weight_int4(w)
+        pack = jq.jq_pack_weight_ternary if fmt == "ternary" else jq.jq_pack_weight_int4
+        self.linear = jq.jq_w158a4_linear if fmt == "ternary" else jq.jq_w4a4_linear
+        self.wq, self.sw = pack(w)
         del w
         self.b = None if self.b_bits is None else jq.bf16_tensor(self.b_bits, "cuda")
         self.y = torch.empty((lin.M, lin.N), dtype=torch.bfloat16, device="cuda")
@@ -87,7 +109,7 @@ class Prepared:
 
 
 def cpu_baseline(preps, target_s):
-    """The oracle as it stands, on a bounded sample of rows of each linear."""
+    """The oracle as it stands, on every row of the workload, repeated until target_s seconds have passed."""
     import numpy as np
     import oracle
     from paper_2609_33601_amd import jq
@@ -101,45 +123,71 @@ def cpu_baseline(preps, target_s):
         cores = 1
     packed = [oracle.pack_weight_int4(p.w_bits) for p in preps]  # offline step, untimed
 
-    def run(nrows):
-        ops = 0
-        outs = []
-        t0 = time.perf_counter()
-        for p, (rq, rs) in zip(preps, packed):
-            n = min(nrows, p.lin.M)
-            rows = np.linspace(0, p.lin.M - 1, n).astype(np.int64)
-            outs.append((rows, oracle.w4a4_linear_rows(p.x_bits, rq, rs, rows, p.b_bits)))
-            ops += 2 * n * p.lin.N * p.lin.K
-        return time.perf_counter() - t0, ops, outs
+    def run():
+        return [oracle.w4a4_linear(p.x_bits, rq, rs, p.b_bits) for p, (rq, rs) in zip(preps, packed)]
 
-    run(8)  # warm-up: thread pools, page faults
-    nrows = 32
-    t, _, _ = run(nrows)
-    nrows = int(max(8, nrows * target_s / max(t, 1e-6)))
-    t, ops, outs = run(nrows)
-    # the sample doubles as a parity check of the GPU outputs on the same rows
-    mism = 0
-    for p, (rows, ref) in zip(preps, outs):
-        got = jq.bf16_bits(p.y[torch_index(rows)])
-        mism += int(np.sum(got != ref))
+    ops_once = sum(2 * p.lin.M * p.lin.N * p.lin.K for p in preps)
+    t0 = time.perf_counter()
+    outs = run()
+    reps = 1
+    while time.perf_counter() - t0 < target_s:
+        run()
+        reps += 1
+    t = time.perf_counter() - t0
+    # the oracle's outputs double as a parity check of every GPU output of the step
+    mism = sum(int(np.sum(jq.bf16_bits(p.y) != ref)) for p, ref in zip(preps, outs))
     return {
-        "value": ops / t / 1e12,
+        "value": reps * ops_once / t / 1e12,
         "unit": "TOPS",
         "cores": int(cores),
         "kind": "oracle",
-        "sample": f"up to {nrows} evenly spaced rows of each of the {len(preps)} linears "
-                  f"({ops / 1e9:.1f} G int ops, {t:.1f} s; weights packed beforehand)",
+        "sample": f"the whole step (every row of the {len(preps)} linears, {ops_once / 1e9:.0f} G int ops) "
+                  f"run {reps} times in {t:.1f} s; weights packed beforehand",
         "seconds": t,
         "host_cpus": os.cpu_count(),
         "affinity_cpus": len(os.sched_getaffinity(0)),
-        "gpu_rows_differing_from_oracle": mism,
+        "gpu_outputs_differing_from_oracle": mism,
     }
 
 
-def torch_index(rows):
-    import torch
+def time_step(torch, preps, steps, warmup):
+    """Average time of one pass over the linears (each a whole quantise + GEMM layer), in us."""
+    stream = torch.cuda.current_stream()
 
-    return torch.from_numpy(rows).cuda()
+    def step():
+        for p in preps:
+            p.linear(p.x, p.wq, p.sw, p.b, y=p.y, workspace=p.ws)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(steps):
+        step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / steps * 1e3
+
+
+def secondary(torch, jq, workloads, steps):
+    cases = [(workloads.FLUX_MLP, "ternary"), (workloads.WORKLOADS["dllm_block"], "int4"),
+             (workloads.WORKLOADS["dllm_block"], "ternary"), (workloads.WORKLOADS["attn_proj"], "int4"),
+             (workloads.WORKLOADS["qkv"], "int4")]
+    out = []
+    for wl, fmt in cases:
+        preps = [Prepared(lin, torch, jq, fmt) for lin in wl.linears]
+        us = time_step(torch, preps, steps, warmup=5)
+        tops = wl.ops / (us * 1e-6) / 1e12
+        layer = "W1.58A4" if fmt == "ternary" else "W4A4"
+        log(f"secondary {wl.name} {layer}: {us:.1f} us/step, {tops:.0f} effective TOPS")
+        out.append({"workload": wl.description, "layer": layer, "us_per_step": us, "effective_TOPS": tops,
+                    "pct_int8_peak": 100.0 * tops / PEAK_INT8_TOPS,
+                    "linears": [{"name": l.name, "M": l.M, "K": l.K, "N": l.N} for l in wl.linears]})
+        del preps
+        torch.cuda.empty_cache()
+    return out
 
 
 def main():
@@ -228,14 +276,18 @@ def main():
         torch.cuda.synchronize()
         del src, dst
 
-    # Re-run the timed configuration once so that y holds the linear's outputs for the parity sample.
+    # Re-run the timed configuration once so that y holds the step's outputs for the oracle comparison.
     step()
     torch.cuda.synchronize()
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(preps, args.cpu_seconds)
         log(f"cpu oracle: {cpu['value']:.4f} TOPS on {cpu['cores']} threads; {cpu['sample']}; "
-            f"gpu/oracle differing outputs on the sample: {cpu['gpu_rows_differing_from_oracle']}")
+            f"gpu/oracle differing outputs: {cpu['gpu_outputs_differing_from_oracle']}")
+
+    sec = None
+    if not args.no_secondary:
+        sec = secondary(torch, jq, workloads, max(10, min(args.steps, 50)))
 
     props = torch.cuda.get_device_properties(0)
     out = {
@@ -263,6 +315,7 @@ def main():
         "roofline": roofline,
         "cpu_baseline": cpu,
         "kernels": kernels,
+        "secondary": sec,
     }
     print(json.dumps(out), flush=True)
 
