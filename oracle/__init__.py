@@ -33,3 +33,16 @@ from .w158a4 import (  # noqa: F401
     w158a4_linear,
     w158a4_linear_rows,
 )
+from .w4a4_group import (  # noqa: F401
+    GROUP_SIZES,
+    quantize_rows_group,
+    quantize_act_group,
+    pack_weight_int4_group,
+    group_code_gemm,
+    group_sum,
+    group_epilogue,
+    w4a4g_gemm_f32,
+    w4a4g_gemm,
+    w4a4g_linear,
+    w4a4g_linear_rows,
+)
