@@ -216,6 +216,96 @@ jq_status jq_w158a4_gemm(const void* q_packed, const float* scale, int64_t M, in
 jq_status jq_w158a4_gemm_i32(const void* q_packed, int64_t M, int64_t K,
                              const void* wt_packed, int64_t N, int32_t* acc, void* stream);
 
+/*
+ * ---------------------------------------------------------------------------
+ * Group-wise W4A4: one scale per G consecutive k (G = 64 or 128).
+ *
+ * The paper's own W4A4 runs quantise in groups along K: group128 for the DiT
+ * and ELF models, group64 for FLUX (appendix experimental-details tables,
+ * quantization-function rows).  The library extends the per-token reading to
+ * groups, on activations and weights alike, per row r and group g:
+ *
+ *     s[r,g]  = fl32(max_{k in g} |x[r,k]| / 7)                (IEEE fp32 division)
+ *     q[r,k]  = clamp(rne(fl32(x[r,k] / s[r,g(k)])), -8, 7),  q = 0 where s = 0
+ *
+ * and the layer sums the exact per-group integer products in k order:
+ *
+ *     acc_g[m,n] = sum_{k in g} qx[m,k] * qw[n,k]                    (exact)
+ *     S[m,n]     = 0;  S = fl32(S + fl32(fl32(fl32(acc_g) * s_x[m,g]) * s_w[n,g]))  for g = 0, 1, ...
+ *     y[m,n]     = bf16_rne(fl32(S + bias[n]))
+ *
+ * each fp32 operation rounded on its own (no fused multiply-add).  Codes use
+ * the packed int4 layout above; scales are fp32 [rows, K/G] row-major.
+ * Shapes: G must be 64 or 128 and K % G == 0, else JQ_ERR_UNSUPPORTED_SHAPE;
+ * for the GEMM calls ceil(M/128) * ceil(N/128) <= 2^26; otherwise the
+ * conventions above apply.
+ */
+
+/*
+ * Group-wise activation quantisation.
+ *   x_bf16   in   [M,K] bf16, 16-byte aligned
+ *   q_packed out  [M,K/2] uint8 (packed int4 layout), 16-byte aligned
+ *   scales   out  [M,K/G] fp32, 4-byte aligned
+ * Errors: JQ_ERR_INVALID_ARG, JQ_ERR_UNSUPPORTED_SHAPE (also M*K > 2^41),
+ * JQ_ERR_MISALIGNED, JQ_ERR_HIP.
+ */
+jq_status jq_quantize_act_group(const void* x_bf16, int64_t M, int64_t K, int64_t G,
+                                void* q_packed, float* scales, void* stream);
+
+/*
+ * Group-wise weight quantisation and packing, once per layer at model load:
+ * the same quantiser on the rows of W [N,K].
+ *   w_bf16 in [N,K] bf16; wq_packed out [N,K/2] uint8; w_scales out [N,K/G] fp32.
+ * Errors: as jq_quantize_act_group.
+ */
+jq_status jq_pack_weight_int4_group(const void* w_bf16, int64_t N, int64_t K, int64_t G,
+                                    void* wq_packed, float* w_scales, void* stream);
+
+/*
+ * Bytes of device workspace jq_w4a4g_linear needs for an [M,K] input in
+ * groups of G: the packed activations (M*K/2 bytes) and their scales
+ * (4*M*K/G bytes), each part rounded up to 256 bytes.  0 for invalid sizes.
+ */
+size_t jq_w4a4g_workspace_bytes(int64_t M, int64_t K, int64_t G);
+
+/*
+ * The whole group-wise W4A4 linear: quantise x in groups into the workspace,
+ * then the group GEMM with the fused epilogue.
+ *   x_bf16       in   [M,K] bf16
+ *   wq_packed    in   [N,K/2] uint8 from jq_pack_weight_int4_group (same G)
+ *   w_scales     in   [N,K/G] fp32 from jq_pack_weight_int4_group
+ *   bias_bf16    in   [N] bf16, or NULL
+ *   y_bf16       out  [M,N] bf16, 16-byte aligned
+ *   workspace    at least jq_w4a4g_workspace_bytes(M,K,G) bytes, 256-byte
+ *                aligned; on return it holds the packed activations followed
+ *                by their scales.
+ * Errors: as jq_quantize_act_group, plus JQ_ERR_WORKSPACE_TOO_SMALL.
+ */
+jq_status jq_w4a4g_linear(const void* x_bf16, int64_t M, int64_t K, int64_t G,
+                          const void* wq_packed, const float* w_scales, int64_t N,
+                          const void* bias_bf16, void* y_bf16,
+                          void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Group GEMM + epilogue on already-quantised activations.
+ *   q_packed, scales   in  [M,K/2] uint8 and [M,K/G] fp32 from jq_quantize_act_group
+ *   other arguments as jq_w4a4g_linear
+ * Errors: JQ_ERR_INVALID_ARG, JQ_ERR_UNSUPPORTED_SHAPE, JQ_ERR_MISALIGNED, JQ_ERR_HIP.
+ */
+jq_status jq_w4a4g_gemm(const void* q_packed, const float* scales, int64_t M, int64_t K, int64_t G,
+                        const void* wq_packed, const float* w_scales, int64_t N,
+                        const void* bias_bf16, void* y_bf16, void* stream);
+
+/*
+ * The fp32 group sum S[m,n] alone (before bias and bf16 rounding), for
+ * checking: the same kernel as jq_w4a4g_gemm with the epilogue replaced by a
+ * plain fp32 store into s_f32 [M,N] (16-byte aligned).
+ * Errors: JQ_ERR_INVALID_ARG, JQ_ERR_UNSUPPORTED_SHAPE, JQ_ERR_MISALIGNED, JQ_ERR_HIP.
+ */
+jq_status jq_w4a4g_gemm_f32(const void* q_packed, const float* scales, int64_t M, int64_t K, int64_t G,
+                            const void* wq_packed, const float* w_scales, int64_t N,
+                            float* s_f32, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

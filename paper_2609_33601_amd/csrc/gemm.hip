@@ -55,31 +55,22 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "gemm_common.h"
 #include "jq_internal.h"
 
 namespace jq {
 
 namespace {
 
-typedef int v4i __attribute__((ext_vector_type(4)));
-typedef __attribute__((address_space(3))) void lds_void_t;
+using namespace gemm_detail;
 
 constexpr int kBM = 128;       // activation rows per block
 constexpr int kBN = 256;       // weight rows per block
-constexpr int kBKB = 64;       // packed bytes of K per stage (128 codes)
-constexpr int kChunks = kBKB / 16;           // 16-byte packed chunks per row per stage
-constexpr int kXChunks = 2 * kChunks;        // 16-byte int8 chunks per activation row per stage
 constexpr int kXSlots = kBM * kXChunks;      // 16-byte slots of the int8 activation tile
-constexpr int kThreads = 256;
 constexpr int kWM = 128, kWN = 64;           // per-wave tile: all activation rows, a quarter of the weight rows
 constexpr int kFM = kWM / 16, kFN = kWN / 16;
 constexpr int kXLoads = kBM * kChunks / kThreads;  // 16-byte activation loads per thread per stage
-constexpr int kGroupM = 8;
-constexpr int kNumXcd = 8;
-constexpr int kBufferFlags = 0x00020000;     // buffer descriptor word 3 for raw byte-addressed loads
-constexpr int kWaitVm0 = (0x7 << 4) | (0xF << 8);  // s_waitcnt vmcnt(0), other counters untouched
 
-static_assert(kChunks == 4 && kXChunks == 8, "swizzles below assume 4 packed / 8 int8 chunks per LDS row");
 static_assert(kXLoads == 2, "activation staging below assumes two loads per thread");
 
 // Weight formats.  kInt4: codes -8..7, two per byte (the W4A4 layer).
@@ -100,22 +91,9 @@ struct WTraits {
   static constexpr int kUnpackValu = kTern ? 7 : 6;    // VALU instructions per widened weight fragment
 };
 
-// LDS slots (16-byte units): chunk c of packed weight row r, and int8 chunk c
-// of activation row r.
-__device__ __forceinline__ int w_slot(int row, int c) { return row * kChunks + (c ^ ((row >> 1) & 3)); }
 // Ternary weight rows are 32 bytes (two chunks); rows 8..15 of every 16 swap
 // their chunks, so the 32 lanes of a ds_read_b64 half cover all 64 banks.
 __device__ __forceinline__ int wt_slot(int row, int c) { return row * 2 + (c ^ ((row >> 3) & 1)); }
-__device__ __forceinline__ int x_slot(int row, int c) { return row * kXChunks + (c ^ (row & 7)); }
-
-__device__ __forceinline__ v4i unpack8(uint32_t p0, uint32_t p1) {
-  v4i r;
-  r[0] = static_cast<int>((p0 << 4) & 0xF0F0F0F0u);
-  r[1] = static_cast<int>(p0 & 0xF0F0F0F0u);
-  r[2] = static_cast<int>((p1 << 4) & 0xF0F0F0F0u);
-  r[3] = static_cast<int>(p1 & 0xF0F0F0F0u);
-  return r;
-}
 
 // Widen 16 ternary codes (one packed dword, code i in bits 2i .. 2i+1) to
 // int8 64 * code: dword d, byte b of the result holds code 4b + d.  Shifting
@@ -140,31 +118,6 @@ __device__ __forceinline__ v4i unpack8_tern_order(uint32_t p0, uint32_t p1) {
   r[2] = static_cast<int>(__builtin_amdgcn_perm(static_cast<uint32_t>(e[2]), static_cast<uint32_t>(e[0]), 0x07050301u));
   r[3] = static_cast<int>(__builtin_amdgcn_perm(static_cast<uint32_t>(e[3]), static_cast<uint32_t>(e[1]), 0x07050301u));
   return r;
-}
-
-// 16 bytes per lane from a buffer straight into LDS: lane i writes dst[i]
-// (buffer_load_dwordx4 ... lds, no registers involved).
-__device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t rs, uint4* dst, uint32_t voffset, int soffset) {
-  __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void_t*)dst, 16, voffset, soffset, 0, 0);
-}
-
-struct TileCoord {
-  int tm, tn;
-};
-
-__device__ __forceinline__ bool tile_of_block(int bid, int tiles_m, int tiles_n, TileCoord* tc) {
-  const int T = tiles_m * tiles_n;
-  const int per_xcd = (T + kNumXcd - 1) / kNumXcd;
-  const int t = (bid % kNumXcd) * per_xcd + bid / kNumXcd;
-  if (t >= T) return false;
-  const int band = kGroupM * tiles_n;
-  const int group = t / band;
-  const int first_m = group * kGroupM;
-  const int gm = min(tiles_m - first_m, kGroupM);
-  const int r = t - group * band;
-  tc->tm = first_m + r % gm;
-  tc->tn = r / gm;
-  return true;
 }
 
 template <WeightFormat WF, Epilogue EPI, bool HAS_BIAS, bool KTAIL>

@@ -179,4 +179,107 @@ jq_status jq_w158a4_gemm_i32(const void* q_packed, int64_t M, int64_t K, const v
   return gemm_i32_common(q_packed, M, K, wt_packed, N, acc, stream, jq::WeightFormat::kTernary);
 }
 
+
+// ---------------------------------------------------------------------------
+// group-wise W4A4
+
+}  // extern "C"
+
+namespace {
+
+jq_status check_group(int64_t rows, int64_t K, int64_t G) {
+  const jq_status st = check_shape(rows, K);
+  if (st != JQ_OK) return st;
+  if ((G != 64 && G != 128) || K % G != 0) return JQ_ERR_UNSUPPORTED_SHAPE;
+  return JQ_OK;
+}
+
+jq_status quantize_group_common(const void* x, int64_t rows, int64_t K, int64_t G, void* q, float* scales,
+                                void* stream) {
+  if (x == nullptr || q == nullptr || scales == nullptr) return JQ_ERR_INVALID_ARG;
+  const jq_status st = check_group(rows, K, G);
+  if (st != JQ_OK) return st;
+  if (rows * K > (int64_t(1) << 41)) return JQ_ERR_UNSUPPORTED_SHAPE;  // the grid counts 2048-element blocks
+  if (!aligned(x, 16) || !aligned(q, 16) || !aligned(scales, 4)) return JQ_ERR_MISALIGNED;
+  return from_hip(jq::launch_quantize_groups(static_cast<const uint16_t*>(x), rows, K, static_cast<int>(G),
+                                             static_cast<uint8_t*>(q), scales, as_stream(stream)));
+}
+
+jq_status check_group_gemm(const void* qx, const float* sx, int64_t M, int64_t K, int64_t G, const void* qw,
+                           const float* sw, int64_t N, const void* bias, const void* y) {
+  if (qx == nullptr || qw == nullptr || y == nullptr || sx == nullptr || sw == nullptr) return JQ_ERR_INVALID_ARG;
+  jq_status st = check_group(M, K, G);
+  if (st != JQ_OK) return st;
+  st = check_group(N, K, G);
+  if (st != JQ_OK) return st;
+  // 32-bit tile indices; 31-bit buffer descriptors over the codes and scales.
+  if (((M + 127) / 128) * ((N + 127) / 128) > (int64_t(1) << 26)) return JQ_ERR_UNSUPPORTED_SHAPE;
+  if (M * (K / 2) >= (int64_t(1) << 31) || N * (K / 2) >= (int64_t(1) << 31)) return JQ_ERR_UNSUPPORTED_SHAPE;
+  if (!aligned(qx, 16) || !aligned(qw, 16) || !aligned(y, 16)) return JQ_ERR_MISALIGNED;
+  if (!aligned(sx, 4) || !aligned(sw, 4)) return JQ_ERR_MISALIGNED;
+  if (bias != nullptr && !aligned(bias, 2)) return JQ_ERR_MISALIGNED;
+  return JQ_OK;
+}
+
+size_t group_workspace_bytes(int64_t M, int64_t K, int64_t G) {
+  if (check_group(M, K, G) != JQ_OK) return 0;
+  return round_up(static_cast<size_t>(M) * static_cast<size_t>(K / 2), kWsAlign) +
+         round_up(static_cast<size_t>(M) * static_cast<size_t>(K / G) * sizeof(float), kWsAlign);
+}
+
+}  // namespace
+
+extern "C" {
+
+jq_status jq_quantize_act_group(const void* x_bf16, int64_t M, int64_t K, int64_t G, void* q_packed, float* scales,
+                                void* stream) {
+  return quantize_group_common(x_bf16, M, K, G, q_packed, scales, stream);
+}
+
+jq_status jq_pack_weight_int4_group(const void* w_bf16, int64_t N, int64_t K, int64_t G, void* wq_packed,
+                                    float* w_scales, void* stream) {
+  return quantize_group_common(w_bf16, N, K, G, wq_packed, w_scales, stream);
+}
+
+size_t jq_w4a4g_workspace_bytes(int64_t M, int64_t K, int64_t G) { return group_workspace_bytes(M, K, G); }
+
+jq_status jq_w4a4g_linear(const void* x_bf16, int64_t M, int64_t K, int64_t G, const void* wq_packed,
+                          const float* w_scales, int64_t N, const void* bias_bf16, void* y_bf16, void* workspace,
+                          size_t workspace_bytes, void* stream) {
+  if (x_bf16 == nullptr || workspace == nullptr) return JQ_ERR_INVALID_ARG;
+  // the activation operands live in the workspace; check the rest with stand-ins
+  jq_status st = check_group_gemm(x_bf16, w_scales, M, K, G, wq_packed, w_scales, N, bias_bf16, y_bf16);
+  if (st != JQ_OK) return st;
+  if (!aligned(workspace, kWsAlign)) return JQ_ERR_MISALIGNED;
+  if (workspace_bytes < group_workspace_bytes(M, K, G)) return JQ_ERR_WORKSPACE_TOO_SMALL;
+  uint8_t* qx = static_cast<uint8_t*>(workspace);
+  float* sx = reinterpret_cast<float*>(qx + round_up(static_cast<size_t>(M) * static_cast<size_t>(K / 2), kWsAlign));
+  hipError_t e = jq::launch_quantize_groups(static_cast<const uint16_t*>(x_bf16), M, K, static_cast<int>(G), qx, sx,
+                                            as_stream(stream));
+  if (e != hipSuccess) return JQ_ERR_HIP;
+  e = jq::launch_w4a4g_gemm(jq::Epilogue::kBf16, qx, sx, M, K, static_cast<int>(G),
+                            static_cast<const uint8_t*>(wq_packed), w_scales, N,
+                            static_cast<const uint16_t*>(bias_bf16), y_bf16, as_stream(stream));
+  return from_hip(e);
+}
+
+jq_status jq_w4a4g_gemm(const void* q_packed, const float* scales, int64_t M, int64_t K, int64_t G,
+                        const void* wq_packed, const float* w_scales, int64_t N, const void* bias_bf16, void* y_bf16,
+                        void* stream) {
+  const jq_status st = check_group_gemm(q_packed, scales, M, K, G, wq_packed, w_scales, N, bias_bf16, y_bf16);
+  if (st != JQ_OK) return st;
+  return from_hip(jq::launch_w4a4g_gemm(jq::Epilogue::kBf16, static_cast<const uint8_t*>(q_packed), scales, M, K,
+                                        static_cast<int>(G), static_cast<const uint8_t*>(wq_packed), w_scales, N,
+                                        static_cast<const uint16_t*>(bias_bf16), y_bf16, as_stream(stream)));
+}
+
+jq_status jq_w4a4g_gemm_f32(const void* q_packed, const float* scales, int64_t M, int64_t K, int64_t G,
+                            const void* wq_packed, const float* w_scales, int64_t N, float* s_f32, void* stream) {
+  const jq_status st = check_group_gemm(q_packed, scales, M, K, G, wq_packed, w_scales, N, nullptr, s_f32);
+  if (st != JQ_OK) return st;
+  return from_hip(jq::launch_w4a4g_gemm(jq::Epilogue::kF32, static_cast<const uint8_t*>(q_packed), scales, M, K,
+                                        static_cast<int>(G), static_cast<const uint8_t*>(wq_packed), w_scales, N,
+                                        nullptr, s_f32, as_stream(stream)));
+}
+
 }  // extern "C"

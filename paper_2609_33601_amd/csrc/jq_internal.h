@@ -22,7 +22,12 @@ hipError_t launch_quantize_rows(const uint16_t* x, int64_t M, int64_t K, uint8_t
 // Ternary weight quantiser: w [N,K] bf16 -> t [N,K/4] 2-bit codes, g [N] fp32.
 hipError_t launch_ternary_rows(const uint16_t* w, int64_t N, int64_t K, uint8_t* t, float* g, hipStream_t st);
 
-enum class Epilogue { kBf16, kInt32 };
+// Group-wise quantiser (G = 64 or 128): x [M,K] bf16 -> q [M,K/2], scale [M, K/G] fp32.
+hipError_t launch_quantize_groups(const uint16_t* x, int64_t M, int64_t K, int G, uint8_t* q, float* scale,
+                                  hipStream_t st);
+
+// kBf16: bf16 output; kInt32: raw accumulators; kF32: the group kernel's fp32 sum before bias.
+enum class Epilogue { kBf16, kInt32, kF32 };
 
 // Weight operand of the GEMM: packed int4 [N,K/2] or packed ternary [N,K/4].
 enum class WeightFormat { kInt4, kTernary };
@@ -33,6 +38,11 @@ enum class WeightFormat { kInt4, kTernary };
 hipError_t launch_w4a4_gemm(Epilogue epi, const uint8_t* qx, const float* sx, int64_t M, int64_t K,
                             const uint8_t* qw, const float* sw, int64_t N, const uint16_t* bias,
                             void* out, hipStream_t st, WeightFormat wf = WeightFormat::kInt4);
+
+// Group-wise GEMM: scales sx [M, K/G] and sw [N, K/G]; epi is kBf16 or kF32.
+hipError_t launch_w4a4g_gemm(Epilogue epi, const uint8_t* qx, const float* sx, int64_t M, int64_t K, int G,
+                             const uint8_t* qw, const float* sw, int64_t N, const uint16_t* bias, void* out,
+                             hipStream_t st);
 
 }  // namespace jq
 

@@ -216,6 +216,46 @@ __global__ __launch_bounds__(256) void quantize_rows_stream_kernel(
   }
 }
 
+// Group-wise variant: one scale per G consecutive k of a row (G = 64 or 128),
+// s[r,g] = fl32(max |x| over the group / 7), the same codes and packing.
+// The matrix is treated as flat 8-element units: thread i loads elements
+// 8i .. 8i+7 (one 16-byte load; a wave reads 1 KiB contiguous) and the
+// G/8 lanes of a group reduce their maxima with shuffles.  Since K % G == 0
+// no group straddles two rows, so the scale of unit i is scale[i / (G/8)]
+// in the row-major [rows, K/G] layout.  The quotient uses the same
+// reciprocal-with-exact-fallback path as the per-row kernel, with one
+// reciprocal per group.
+template <int G>
+__global__ __launch_bounds__(256) void quantize_groups_kernel(const uint16_t* __restrict__ x, int64_t units,
+                                                              uint8_t* __restrict__ q, float* __restrict__ scale) {
+  constexpr int kLanes = G / 8;
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  const bool live = i < units;
+  uint4 v = make_uint4(0, 0, 0, 0);
+  if (live) v = reinterpret_cast<const uint4*>(x)[i];
+  u16x2 am = __builtin_bit_cast(u16x2, v.x & 0x7FFF7FFFu);
+  am = __builtin_elementwise_max(am, __builtin_bit_cast(u16x2, v.y & 0x7FFF7FFFu));
+  am = __builtin_elementwise_max(am, __builtin_bit_cast(u16x2, v.z & 0x7FFF7FFFu));
+  am = __builtin_elementwise_max(am, __builtin_bit_cast(u16x2, v.w & 0x7FFF7FFFu));
+  uint32_t amax = am.x > am.y ? am.x : am.y;
+#pragma unroll
+  for (int off = 1; off < kLanes; off <<= 1) {
+    const uint32_t o = static_cast<uint32_t>(__shfl_xor(static_cast<int>(amax), off, 64));
+    amax = amax > o ? amax : o;
+  }
+  const float a = __uint_as_float(amax << 16);
+  const float s = a / 7.0f;
+  if (live && (threadIdx.x % kLanes) == 0) scale[i / kLanes] = s;
+  uint32_t p = 0;
+  if (s != 0.0f) {
+    const float rcp = 1.0f / s;
+    bool near = true;
+    if (!__builtin_isinf(rcp)) p = pack8_fast(v, rcp, &near);
+    if (near) p = pack8_exact(v, s);
+  }
+  if (live) reinterpret_cast<uint32_t*>(q)[i] = p;
+}
+
 template <int NC>
 hipError_t launch_nc(const uint16_t* x, int64_t M, int64_t K, uint8_t* q, float* s, int waves, hipStream_t st) {
   hipLaunchKernelGGL(quantize_rows_kernel<NC>, dim3(static_cast<unsigned>(M)), dim3(64 * waves), 0, st, x, M, K,
@@ -243,6 +283,18 @@ hipError_t launch_quantize_rows(const uint16_t* x, int64_t M, int64_t K, uint8_t
   }
   const dim3 grid(static_cast<unsigned>((M + 3) / 4));
   hipLaunchKernelGGL(quantize_rows_stream_kernel, grid, dim3(256), 0, st, x, M, K, q, s);
+  return hipGetLastError();
+}
+
+hipError_t launch_quantize_groups(const uint16_t* x, int64_t M, int64_t K, int G, uint8_t* q, float* s,
+                                  hipStream_t st) {
+  const int64_t units = M * K / 8;
+  const dim3 grid(static_cast<unsigned>((units + 255) / 256));
+  if (G == 64) {
+    hipLaunchKernelGGL(quantize_groups_kernel<64>, grid, dim3(256), 0, st, x, units, q, s);
+  } else {
+    hipLaunchKernelGGL(quantize_groups_kernel<128>, grid, dim3(256), 0, st, x, units, q, s);
+  }
   return hipGetLastError();
 }
 

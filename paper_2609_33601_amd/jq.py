@@ -34,6 +34,12 @@ SIGNATURES = {
     "jq_w158a4_linear": (ctypes.c_int, [_vp, _i64, _i64, _vp, _fp, _i64, _vp, _vp, _vp, _sz, _vp]),
     "jq_w158a4_gemm": (ctypes.c_int, [_vp, _fp, _i64, _i64, _vp, _fp, _i64, _vp, _vp, _vp]),
     "jq_w158a4_gemm_i32": (ctypes.c_int, [_vp, _i64, _i64, _vp, _i64, _ip, _vp]),
+    "jq_quantize_act_group": (ctypes.c_int, [_vp, _i64, _i64, _i64, _vp, _fp, _vp]),
+    "jq_pack_weight_int4_group": (ctypes.c_int, [_vp, _i64, _i64, _i64, _vp, _fp, _vp]),
+    "jq_w4a4g_workspace_bytes": (_sz, [_i64, _i64, _i64]),
+    "jq_w4a4g_linear": (ctypes.c_int, [_vp, _i64, _i64, _i64, _vp, _fp, _i64, _vp, _vp, _vp, _sz, _vp]),
+    "jq_w4a4g_gemm": (ctypes.c_int, [_vp, _fp, _i64, _i64, _i64, _vp, _fp, _i64, _vp, _vp, _vp]),
+    "jq_w4a4g_gemm_f32": (ctypes.c_int, [_vp, _fp, _i64, _i64, _i64, _vp, _fp, _i64, _fp, _vp]),
 }
 
 _lib = None
@@ -259,6 +265,92 @@ def jq_w158a4_gemm_i32(q, wt, acc=None, stream=None):
                                   _dev(acc, torch.int32, (M, N), "acc"), _stream_ptr(stream))
     _check(st, "jq_w158a4_gemm_i32")
     return acc
+
+
+# ---------------------------------------------------------------------------
+# group-wise W4A4: scales [rows, K/G], G = 64 or 128
+# ---------------------------------------------------------------------------
+
+
+def jq_w4a4g_workspace_bytes(M, K, G):
+    return int(lib().jq_w4a4g_workspace_bytes(int(M), int(K), int(G)))
+
+
+def _quantize_group(fn, name, x, G, q, scale, stream):
+    torch = _torch()
+    R, K = x.shape
+    if q is None:
+        q = torch.empty((R, K // 2), dtype=torch.uint8, device=x.device)
+    if scale is None:
+        scale = torch.empty((R, K // G), dtype=torch.float32, device=x.device)
+    st = fn(_dev(x, torch.bfloat16, None, "x"), R, K, G, _dev(q, torch.uint8, (R, K // 2), "q"),
+            _dev(scale, torch.float32, (R, K // G), "scale"), _stream_ptr(stream))
+    _check(st, name)
+    return q, scale
+
+
+def jq_quantize_act_group(x, G, q=None, scale=None, stream=None):
+    """x bf16 [M,K] -> (q uint8 [M,K/2], scales fp32 [M,K/G])."""
+    return _quantize_group(lib().jq_quantize_act_group, "jq_quantize_act_group", x, G, q, scale, stream)
+
+
+def jq_pack_weight_int4_group(w, G, wq=None, w_scale=None, stream=None):
+    """w bf16 [N,K] -> (wq uint8 [N,K/2], w_scales fp32 [N,K/G])."""
+    return _quantize_group(lib().jq_pack_weight_int4_group, "jq_pack_weight_int4_group", w, G, wq, w_scale, stream)
+
+
+def jq_w4a4g_linear(x, wq, w_scale, G, bias=None, y=None, workspace=None, stream=None):
+    """y = group-wise W4A4 linear of x (bf16 [M,K]); returns bf16 [M,N]."""
+    torch = _torch()
+    M, K = x.shape
+    N = wq.shape[0]
+    if y is None:
+        y = torch.empty((M, N), dtype=torch.bfloat16, device=x.device)
+    if workspace is None:
+        workspace = torch.empty((jq_w4a4g_workspace_bytes(M, K, G),), dtype=torch.uint8, device=x.device)
+    bptr = ctypes.c_void_p(None) if bias is None else _dev(bias, torch.bfloat16, (N,), "bias")
+    st = lib().jq_w4a4g_linear(_dev(x, torch.bfloat16, None, "x"), M, K, G,
+                               _dev(wq, torch.uint8, (N, K // 2), "wq"),
+                               _dev(w_scale, torch.float32, (N, K // G), "w_scale"), N, bptr,
+                               _dev(y, torch.bfloat16, (M, N), "y"),
+                               _dev(workspace, torch.uint8, None, "workspace"), workspace.numel(),
+                               _stream_ptr(stream))
+    _check(st, "jq_w4a4g_linear")
+    return y
+
+
+def jq_w4a4g_gemm(q, scale, wq, w_scale, G, bias=None, y=None, stream=None):
+    """Group GEMM + epilogue on pre-quantised activations; returns bf16 [M,N]."""
+    torch = _torch()
+    M, Kh = q.shape
+    K = 2 * Kh
+    N = wq.shape[0]
+    if y is None:
+        y = torch.empty((M, N), dtype=torch.bfloat16, device=q.device)
+    bptr = ctypes.c_void_p(None) if bias is None else _dev(bias, torch.bfloat16, (N,), "bias")
+    st = lib().jq_w4a4g_gemm(_dev(q, torch.uint8, (M, Kh), "q"), _dev(scale, torch.float32, (M, K // G), "scale"),
+                             M, K, G, _dev(wq, torch.uint8, (N, Kh), "wq"),
+                             _dev(w_scale, torch.float32, (N, K // G), "w_scale"), N, bptr,
+                             _dev(y, torch.bfloat16, (M, N), "y"), _stream_ptr(stream))
+    _check(st, "jq_w4a4g_gemm")
+    return y
+
+
+def jq_w4a4g_gemm_f32(q, scale, wq, w_scale, G, out=None, stream=None):
+    """The fp32 group sum S [M,N] (before bias and bf16 rounding)."""
+    torch = _torch()
+    M, Kh = q.shape
+    K = 2 * Kh
+    N = wq.shape[0]
+    if out is None:
+        out = torch.empty((M, N), dtype=torch.float32, device=q.device)
+    st = lib().jq_w4a4g_gemm_f32(_dev(q, torch.uint8, (M, Kh), "q"),
+                                 _dev(scale, torch.float32, (M, K // G), "scale"), M, K, G,
+                                 _dev(wq, torch.uint8, (N, Kh), "wq"),
+                                 _dev(w_scale, torch.float32, (N, K // G), "w_scale"), N,
+                                 _dev(out, torch.float32, (M, N), "out"), _stream_ptr(stream))
+    _check(st, "jq_w4a4g_gemm_f32")
+    return out
 
 
 # ---------------------------------------------------------------------------

@@ -31,7 +31,7 @@ def header_functions():
 
 def test_exports_every_declared_symbol():
     names = header_functions()
-    assert len(names) == 12, names
+    assert len(names) == 18, names
     lib = ctypes.CDLL(jq.LIB_PATH)
     for n in names:
         assert hasattr(lib, n), f"libjq.so does not export {n}"
@@ -117,6 +117,51 @@ def test_gemm_validation(fmt):
     # 2 GiB packed weights: N*K/2 bytes for int4, N*K/4 for ternary
     big_n = (1 << 16) if fmt == "w4a4" else (1 << 17)
     assert i(A, 64, 65536, A, big_n, A, None) == jq.JQ_ERR_UNSUPPORTED_SHAPE
+
+
+def test_group_workspace_bytes():
+    L = jq.lib()
+    assert L.jq_w4a4g_workspace_bytes(4608, 3072, 64) == 4608 * 1536 + 4608 * 48 * 4
+    assert L.jq_w4a4g_workspace_bytes(1, 128, 128) == 256 + 256
+    assert L.jq_w4a4g_workspace_bytes(8, 192, 128) == 0   # K % G != 0
+    assert L.jq_w4a4g_workspace_bytes(8, 128, 32) == 0    # unsupported group size
+    assert L.jq_w4a4g_workspace_bytes(0, 128, 64) == 0
+
+
+@pytest.mark.parametrize("fn", ["jq_quantize_act_group", "jq_pack_weight_int4_group"])
+def test_group_quantize_validation(fn):
+    f = getattr(jq.lib(), fn)
+    assert f(None, 8, 128, 64, A, A, None) == jq.JQ_ERR_INVALID_ARG
+    assert f(A, 8, 128, 64, None, A, None) == jq.JQ_ERR_INVALID_ARG
+    assert f(A, 8, 128, 64, A, None, None) == jq.JQ_ERR_INVALID_ARG
+    assert f(A, 0, 128, 64, A, A, None) == jq.JQ_ERR_INVALID_ARG
+    for K, G in ((192, 128), (128, 32), (128, 0), (128, 256), (100, 64)):
+        assert f(A, 8, K, G, A, A, None) == jq.JQ_ERR_UNSUPPORTED_SHAPE, (K, G)
+    assert f(A, 1 << 30, 65536, 64, A, A, None) == jq.JQ_ERR_UNSUPPORTED_SHAPE
+    assert f(MIS, 8, 128, 64, A, A, None) == jq.JQ_ERR_MISALIGNED
+    assert f(A, 8, 128, 64, A + 8, A, None) == jq.JQ_ERR_MISALIGNED
+    assert f(A, 8, 128, 64, A, A + 2, None) == jq.JQ_ERR_MISALIGNED
+
+
+def test_group_gemm_validation():
+    L = jq.lib()
+    g, f32 = L.jq_w4a4g_gemm, L.jq_w4a4g_gemm_f32
+    for k in range(5):
+        args = [A, A, 4, 128, 64, A, A, 4, None, A, None]
+        args[[0, 1, 5, 6, 9][k]] = None
+        assert g(*args) == jq.JQ_ERR_INVALID_ARG, k
+    assert g(A, A, 4, 192, 128, A, A, 4, None, A, None) == jq.JQ_ERR_UNSUPPORTED_SHAPE
+    assert g(A, A, 4, 128, 64, A, A, 4, A + 1, A, None) == jq.JQ_ERR_MISALIGNED
+    assert g(A, A + 2, 4, 128, 64, A, A, 4, None, A, None) == jq.JQ_ERR_MISALIGNED
+    assert f32(A, A, 4, 128, 64, A, A, 4, None, None) == jq.JQ_ERR_INVALID_ARG
+    assert f32(A, A, 4, 128, 64, A, A, 4, A + 8, None) == jq.JQ_ERR_MISALIGNED
+    assert f32(A, A, 1 << 20, 4096, 64, A, A, 64, A, None) == jq.JQ_ERR_UNSUPPORTED_SHAPE
+    lin = L.jq_w4a4g_linear
+    need = L.jq_w4a4g_workspace_bytes(16, 128, 64)
+    assert lin(A, 16, 128, 64, A, A, 32, None, A, A, need - 1, None) == jq.JQ_ERR_WORKSPACE_TOO_SMALL
+    assert lin(A, 16, 128, 64, A, A, 32, None, A, A + 16, need, None) == jq.JQ_ERR_MISALIGNED
+    assert lin(A, 16, 128, 64, A, A, 32, None, A, None, need, None) == jq.JQ_ERR_INVALID_ARG
+    assert lin(A, 16, 192, 128, A, A, 32, None, A, A, need, None) == jq.JQ_ERR_UNSUPPORTED_SHAPE
 
 
 def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
