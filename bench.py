@@ -15,9 +15,9 @@ events on the stream the library launches on, and the CPU oracle timed on a
 the whole step on the host cores (repeated until about ten seconds have passed).
 
 `secondary` reports, from the same run, the same measurement for other
-layers: the FLUX MLP step with ternary weights (W1.58A4), the 8B
-diffusion-LLM block linears (W4A4 and W1.58A4) and the DiT attention
-projection and fused QKV linears.
+layers: the FLUX MLP step with ternary weights (W1.58A4) and group-wise
+(group64), the 8B diffusion-LLM block linears (W4A4, W1.58A4, group128) and
+the DiT attention projection and fused QKV linears.
 """
 
 import argparse
@@ -86,7 +86,8 @@ def _make_x(lin):
 class Prepared:
     """Device-resident inputs, packed weight and output/workspace buffers of one linear.
 
-    fmt "int4" packs the weight for the W4A4 layer, "ternary" for W1.58A4.
+    fmt "int4" packs the weight for the W4A4 layer, "ternary" for W1.58A4,
+    "group64" / "group128" for group-wise W4A4 with that group size.
     """
 
     def __init__(self, lin, torch, jq, fmt="int4"):
@@ -97,13 +98,21 @@ class Prepared:
         self.b_bits = lin.make_bias()
         self.x = jq.bf16_tensor(self.x_bits, "cuda")
         w = jq.bf16_tensor(self.w_bits, "cuda")
-        pack = jq.jq_pack_weight_ternary if fmt == "ternary" else jq.jq_pack_weight_int4
-        self.linear = jq.jq_w158a4_linear if fmt == "ternary" else jq.jq_w4a4_linear
-        self.wq, self.sw = pack(w)
+        ws_bytes = jq.jq_w4a4_workspace_bytes(lin.M, lin.K)
+        if fmt.startswith("group"):
+            G = int(fmt[5:])
+            self.wq, self.sw = jq.jq_pack_weight_int4_group(w, G)
+            self.linear = lambda x, wq, sw, b, y, workspace: jq.jq_w4a4g_linear(x, wq, sw, G, b, y=y,
+                                                                               workspace=workspace)
+            ws_bytes = jq.jq_w4a4g_workspace_bytes(lin.M, lin.K, G)
+        else:
+            pack = jq.jq_pack_weight_ternary if fmt == "ternary" else jq.jq_pack_weight_int4
+            self.linear = jq.jq_w158a4_linear if fmt == "ternary" else jq.jq_w4a4_linear
+            self.wq, self.sw = pack(w)
         del w
         self.b = None if self.b_bits is None else jq.bf16_tensor(self.b_bits, "cuda")
         self.y = torch.empty((lin.M, lin.N), dtype=torch.bfloat16, device="cuda")
-        self.ws = torch.empty(jq.jq_w4a4_workspace_bytes(lin.M, lin.K), dtype=torch.uint8, device="cuda")
+        self.ws = torch.empty(ws_bytes, dtype=torch.uint8, device="cuda")
         self.q = torch.empty((lin.M, lin.K // 2), dtype=torch.uint8, device="cuda")
         self.s = torch.empty((lin.M,), dtype=torch.float32, device="cuda")
 
@@ -174,13 +183,14 @@ def time_step(torch, preps, steps, warmup):
 def secondary(torch, jq, workloads, steps):
     cases = [(workloads.FLUX_MLP, "ternary"), (workloads.WORKLOADS["dllm_block"], "int4"),
              (workloads.WORKLOADS["dllm_block"], "ternary"), (workloads.WORKLOADS["attn_proj"], "int4"),
-             (workloads.WORKLOADS["qkv"], "int4")]
+             (workloads.WORKLOADS["qkv"], "int4"), (workloads.FLUX_MLP, "group64"),
+             (workloads.WORKLOADS["dllm_block"], "group128")]
     out = []
     for wl, fmt in cases:
         preps = [Prepared(lin, torch, jq, fmt) for lin in wl.linears]
         us = time_step(torch, preps, steps, warmup=5)
         tops = wl.ops / (us * 1e-6) / 1e12
-        layer = "W1.58A4" if fmt == "ternary" else "W4A4"
+        layer = {"ternary": "W1.58A4", "int4": "W4A4"}.get(fmt, f"W4A4 {fmt}")
         log(f"secondary {wl.name} {layer}: {us:.1f} us/step, {tops:.0f} effective TOPS")
         out.append({"workload": wl.description, "layer": layer, "us_per_step": us, "effective_TOPS": tops,
                     "pct_int8_peak": 100.0 * tops / PEAK_INT8_TOPS,
