@@ -306,6 +306,99 @@ jq_status jq_w4a4g_gemm_f32(const void* q_packed, const float* scales, int64_t M
                             const void* wq_packed, const float* w_scales, int64_t N,
                             float* s_f32, void* stream);
 
+/* ------------------------------------------------------------------------
+ * BF6 engine: the same W4A4 layer (Sec. 3.1; FAQ Q7: quantisation, packing
+ * and low-bit matrix-multiplication kernels) computed on gfx950's 6-bit
+ * matrix cores.  Every int4 code -8..7 is exactly representable in the BF6
+ * (E3M2) format and every partial sum of the contraction is an integer below
+ * 2^22, so the fp32 accumulators equal the exact integer ones: codes, scales,
+ * accumulators and bf16 outputs are identical to the packed-int4 calls above.
+ *
+ * BF6 operand layout (activations and weights alike), 6 bits per code:
+ *   - a code c is encoded as sign bit 5 and the E3M2 magnitude
+ *     |c| = (1 + m/4) * 2^(e-3) (e in bits 4..2, m in bits 1..0; 0 -> 0);
+ *   - 32 codes c[0..31] form a 192-bit group, code p in bits 6p..6p+5
+ *     (six little-endian dwords);
+ *   - rows are padded with zero codes to a multiple of 32 and taken in bands
+ *     of 32; K is padded with zero codes to a multiple of 128 and cut into
+ *     KS = 2*ceil(K/128) k-steps of 64 codes;
+ *   - the fragment of band b and k-step s is 1536 bytes at (b*KS + s)*1536;
+ *     its bytes 24L..24L+23 (L = r + 32h, r < 32, h < 2) hold the group of
+ *     codes 64s+32h .. 64s+32h+31 of row 32b + r.
+ * Size: jq_f6_operand_bytes(rows, K) = ceil(rows/32) * KS * 1536.
+ *
+ * Shapes, alignment and errors follow the conventions at the top of this
+ * file, with each BF6 operand below 2^31 bytes.
+ * ------------------------------------------------------------------------ */
+
+/* Bytes of the BF6 operand of a [rows,K] matrix (0 for invalid sizes). */
+size_t jq_f6_operand_bytes(int64_t rows, int64_t K);
+
+/*
+ * Activation quantisation into the BF6 operand (Sec. 3.1; FAQ Q7): the
+ * quantiser of jq_quantize_act (same scale, same codes) written in the BF6
+ * layout; padding rows get zero codes.
+ *   x_bf16  in   [M,K] bf16, 16-byte aligned
+ *   xf6     out  jq_f6_operand_bytes(M,K) bytes, 16-byte aligned
+ *   scale   out  [M] fp32
+ * Errors: as jq_quantize_act.
+ */
+jq_status jq_quantize_act_f6(const void* x_bf16, int64_t M, int64_t K,
+                             void* xf6, float* scale, void* stream);
+
+/*
+ * Re-encode packed int4 codes (any codes -8..7) as a BF6 operand; lossless.
+ * For weights this is done once per layer at model load, after
+ * jq_pack_weight_int4, whose scales stay the weight scales.  Also serves
+ * activation codes from jq_quantize_act.
+ *   q_packed in   [rows,K/2] uint8, 16-byte aligned
+ *   f6       out  jq_f6_operand_bytes(rows,K) bytes, 16-byte aligned
+ *            (padding rows and codes are written as zeros)
+ * Errors: JQ_ERR_INVALID_ARG, JQ_ERR_UNSUPPORTED_SHAPE, JQ_ERR_MISALIGNED, JQ_ERR_HIP.
+ */
+jq_status jq_int4_to_f6(const void* q_packed, int64_t rows, int64_t K, void* f6, void* stream);
+
+/*
+ * Bytes of device workspace jq_w4a4_f6_linear needs for an [M,K] input: the
+ * BF6 activation operand and the scales (4*M bytes), each part rounded up to
+ * 256 bytes.  0 for invalid sizes.
+ */
+size_t jq_w4a4_f6_workspace_bytes(int64_t M, int64_t K);
+
+/*
+ * The whole W4A4 linear on the BF6 engine: quantise x per token into the
+ * workspace (BF6 operand, then scales), then the GEMM with the fused epilogue
+ * y = bf16_rne(((fl32(acc) * s_x[m]) * s_w[n]) + bias[n]).
+ *   x_bf16      in   [M,K] bf16
+ *   wf6         in   BF6 weight operand from jq_int4_to_f6
+ *   w_scale     in   [N] fp32 from jq_pack_weight_int4
+ *   bias_bf16   in   [N] bf16, or NULL
+ *   y_bf16      out  [M,N] bf16, 16-byte aligned
+ *   workspace   at least jq_w4a4_f6_workspace_bytes(M,K) bytes, 256-byte aligned
+ * Errors: as jq_w4a4_linear.
+ */
+jq_status jq_w4a4_f6_linear(const void* x_bf16, int64_t M, int64_t K,
+                            const void* wf6, const float* w_scale, int64_t N,
+                            const void* bias_bf16, void* y_bf16,
+                            void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * GEMM + epilogue of the BF6 engine on an already-quantised activation
+ * operand (from jq_quantize_act_f6 or jq_int4_to_f6) and its scales.
+ * Errors: JQ_ERR_INVALID_ARG, JQ_ERR_UNSUPPORTED_SHAPE, JQ_ERR_MISALIGNED, JQ_ERR_HIP.
+ */
+jq_status jq_w4a4_f6_gemm(const void* xf6, const float* scale, int64_t M, int64_t K,
+                          const void* wf6, const float* w_scale, int64_t N,
+                          const void* bias_bf16, void* y_bf16, void* stream);
+
+/*
+ * The exact contraction alone on the BF6 engine, for checking:
+ * acc [M,N] int32 (16-byte aligned) = sum_k qx[m,k] * qw[n,k].
+ * Errors: as jq_w4a4_f6_gemm.
+ */
+jq_status jq_w4a4_f6_gemm_i32(const void* xf6, int64_t M, int64_t K,
+                              const void* wf6, int64_t N, int32_t* acc, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

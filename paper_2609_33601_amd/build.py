@@ -9,7 +9,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libjq.so")
-SOURCES = ["quantize.hip", "ternary.hip", "gemm.hip", "gemm_group.hip", "jq_api.cpp"]
+SOURCES = ["quantize.hip", "ternary.hip", "gemm.hip", "gemm_group.hip", "f6.hip", "jq_api.cpp"]
 ARCH = "gfx950"
 
 HIPCC_FLAGS = [

@@ -1,0 +1,545 @@
+// The W4A4 layer on gfx950's 6-bit matrix cores (v_mfma_scale_f32_32x32x64_f8f6f4
+// with BF6 = E3M2 operands), an exact alternative to the int8 MFMA path.
+//
+// Why it is exact.  Every int4 code -8..7 is a BF6 E3M2 value (|c| = 1.m * 2^e
+// with two mantissa bits and e <= 3), so the matrix core multiplies the codes
+// exactly.  Each product is an integer of magnitude <= 64 and every partial sum
+// of a row of K <= 65536 products is an integer below 2^22, which fp32 holds
+// exactly whatever the order of the additions.  The fp32 accumulator therefore
+// equals the integer contraction acc[m,n] = sum_k qx[m,k] * qw[n,k], and the
+// epilogue ((acc * s_x) * s_w) + bias sees the same operands as on the int8
+// path.  Outputs are bit-identical to it.
+//
+// Why it is faster.  gfx950 issues the 6-bit MFMA at twice the int8 rate, and the
+// operands reach it already encoded, so the loop holds no widening
+// arithmetic at all:
+//   * activations are quantised straight into BF6 by quantize_rows_f6_kernel
+//     (the same scale and codes as the packed-int4 quantiser);
+//   * weights are converted once, offline, from the canonical packed int4
+//     codes into a fragment-major BF6 layout.
+//
+// BF6 operand layout (activations and weights alike).  32 codes c[0..31] form
+// a group of 192 bits, code p in bits 6p .. 6p+5 (six little-endian dwords
+// d0..d5).  Rows are padded with zero codes to a multiple of 32 and taken in
+// bands of 32; K is padded with zero codes to a multiple of 128 and cut into
+// k-steps of 64 codes (KS of them).  The fragment of band b and k-step s is
+// 1536 contiguous bytes at (b * KS + s) * 1536; lane L = r + 32h of it is the
+// group of codes 64s + 32h .. 64s + 32h + 31 of row 32b + r, with d0..d3 at
+// byte 16L and d4, d5 at byte 1024 + 8L.  That is one lane of a
+// v_mfma_*_32x32x64_f8f6f4 operand (lane L: row L % 32, one 32-code half
+// L / 32 of the instruction's 64 codes of K); A and B lanes use the same
+// assignment, so the contraction is summed correctly.  A wave loads a
+// fragment with one fully coalesced 16-byte and one 8-byte access per lane,
+// into one register tuple.
+//
+// GEMM structure.  Block tile 256 (m) x 256 (n), one block per CU, four waves,
+// one per SIMD.  Wave w owns weight rows 64w .. 64w+63 of the tile (two bands)
+// and every activation row: 2 x 8 tiles of 32x32, i.e. 256 fp32 accumulators
+// per lane, which gfx950 holds in its accumulation registers beside 256
+// ordinary VGPRs.
+//   * Activations: shared by the four waves, staged through LDS.  A stage is
+//     128 codes of K (two k-steps x eight bands = 16 fragments, 24 KiB), moved
+//     from global memory by buffer_load ... lds (no registers) into a ring of
+//     four stage slots, three stages ahead.  The 8-byte part of a fragment
+//     lane is read from LDS as 16 bytes (the upper half is ignored by the
+//     6-bit MFMA), so that no two fragments' reads can be fused into one
+//     instruction whose result would then have to be copied apart.
+//   * Weights: private to a wave, loaded straight into registers two stages
+//     ahead (a ring of three register sets, so the stage loop is unrolled by 3).
+//   * Per stage: the sixteen activation fragments roll through a window of
+//     four registers sets (fragment i is read while the MFMAs of fragment
+//     i - 4 run).  Half-way through the stage the wave waits for its share of
+//     the next stage's DMA, meets the others at a barrier (no memory fence),
+//     and issues the weight loads and DMA of the stages ahead.  No VALU work
+//     sits between the MFMAs.
+//   * The weight fragment is operand A and the activation fragment operand B,
+//     so the 32x32 result is y^T: lane L holds column m = L % 32 and rows
+//     n = 8j + 4(L / 32) + r (j, r = 0..3), i.e. four consecutive outputs of
+//     one row per j, stored as one 8-byte bf16 write.
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <type_traits>
+
+#include "gemm_common.h"
+#include "jq_internal.h"
+
+namespace jq {
+
+namespace {
+
+using namespace gemm_detail;
+
+typedef int v8i __attribute__((ext_vector_type(8)));
+typedef float v16f __attribute__((ext_vector_type(16)));
+typedef unsigned v6u __attribute__((ext_vector_type(6)));
+typedef float v16f32 __attribute__((ext_vector_type(16)));
+typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
+
+constexpr int kFragBytes = 1536;          // one 32-row x 64-code fragment
+constexpr int kFBM = 256, kFBN = 256;     // block tile
+constexpr int kStageBytes = 2 * 8 * kFragBytes;      // 24 KiB: two k-steps x eight bands
+constexpr int kStageU4 = kStageBytes / 16;
+constexpr int kF6Threads = 512;                       // eight waves, two per SIMD
+constexpr int kDmaPerWave = kStageU4 / 64 / (kF6Threads / 64);  // 3 DMA instructions per wave per stage
+
+static_assert(kDmaPerWave == 3, "stage DMA split assumes 3 instructions per wave");
+
+// 32 codes (as exact fp32 integers, code p in q[p]) -> six dwords, code p in bits 6p..6p+5.
+// The converter interleaves its two sources (field 2i <- src0[i], field 2i+1 <- src1[i]).
+__device__ __forceinline__ v6u bf6_group(const float* q) {
+  v16f32 ev, od;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    ev[i] = q[2 * i];
+    od[i] = q[2 * i + 1];
+  }
+  return __builtin_amdgcn_cvt_scalef32_2xpk16_bf6_f32(ev, od, 1.0f);
+}
+
+constexpr float kMagic = 12582912.0f;         // 1.5 * 2^23
+constexpr float kNearTie = 0.5f - 0x1p-17f;
+
+__device__ __forceinline__ float bf16_lo(uint32_t u) { return __uint_as_float(u << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t u) { return __uint_as_float(u & 0xFFFF0000u); }
+
+// Codes of one 32-element group (16 dwords of bf16 pairs).  Reciprocal path
+// with the exact IEEE division wherever the product sits next to a rounding
+// decision point (the argument is that of the packed-int4 quantiser), or the
+// division for every element when the reciprocal overflows.
+__device__ __forceinline__ void codes32(const uint32_t* w, float s, float rcp, bool exact_row, float* q) {
+  bool near = exact_row;
+  if (!exact_row) {
+    float dmax = 0.0f;
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      const float te = bf16_lo(w[j]) * rcp;
+      const float to = bf16_hi(w[j]) * rcp;
+      const float re = (te + kMagic) - kMagic;
+      const float ro = (to + kMagic) - kMagic;
+      dmax = fmaxf(dmax, fmaxf(fabsf(te - re), fabsf(to - ro)));
+      q[2 * j] = re;
+      q[2 * j + 1] = ro;
+    }
+    near = !(dmax < kNearTie);
+  }
+  if (near) {
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      q[2 * j] = fminf(fmaxf(__builtin_rintf(bf16_lo(w[j]) / s), -8.0f), 7.0f);
+      q[2 * j + 1] = fminf(fmaxf(__builtin_rintf(bf16_hi(w[j]) / s), -8.0f), 7.0f);
+    }
+  }
+}
+
+// Store the BF6 group gi (= 2 * kstep + half) of row `row` into the operand layout.
+__device__ __forceinline__ void store_group(uint8_t* out, int64_t ksteps, int64_t row, int gi, v6u d) {
+  const int s = gi >> 1, h = gi & 1;
+  const int L = static_cast<int>(row & 31) + 32 * h;
+  uint8_t* p = out + ((row >> 5) * ksteps + s) * kFragBytes;
+  *reinterpret_cast<uint4*>(p + 16 * L) = make_uint4(d[0], d[1], d[2], d[3]);
+  *reinterpret_cast<uint2*>(p + 1024 + 8 * L) = make_uint2(d[4], d[5]);
+}
+
+// Row of block b.  Blocks are dealt round-robin to the 8 XCDs; the 32 rows of
+// a band all go to the blocks of one XCD, so the partial cache lines of a
+// fragment are completed in one L2 before they are written back.
+__device__ __forceinline__ int64_t row_of_block(int64_t b) {
+  const int64_t x = b % kNumXcd, j = b / kNumXcd;
+  return 32 * (kNumXcd * (j / 32) + x) + (j % 32);
+}
+
+// Per-token quantiser writing the BF6 operand.  One block per row of the
+// padded operand; thread i handles groups i + T j (j < NJ) of 32 codes, each
+// read with four 16-byte loads, and keeps them in registers between the
+// absmax and the quantisation.  The scale and the codes are those of
+// quantize_rows_kernel.  Padding rows (M <= row < 32 * ceil(M/32)) get zero
+// codes and no scale.
+template <int NJ>
+__global__ __launch_bounds__(512) void quantize_rows_f6_kernel(const uint16_t* __restrict__ x, int64_t M, int64_t K,
+                                                               int64_t rows_padded, int64_t ksteps,
+                                                               uint8_t* __restrict__ out, float* __restrict__ scale) {
+  __shared__ uint32_t wave_max[8];
+  const int T = blockDim.x;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nwaves = T >> 6;
+  const int64_t row = row_of_block(blockIdx.x);
+  if (row >= rows_padded) return;
+  const bool live = row < M;
+  const int groups = static_cast<int>(2 * ksteps);
+  const uint16_t* xr = x + (live ? row : 0) * K;
+
+  uint4 v[NJ][4];
+  u16x2 am = {0, 0};
+#pragma unroll
+  for (int j = 0; j < NJ; ++j) {
+    const int64_t k = 32 * static_cast<int64_t>(threadIdx.x + T * j);
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      v[j][c] = (live && k < K) ? *reinterpret_cast<const uint4*>(xr + k + 8 * c) : make_uint4(0, 0, 0, 0);
+      am = __builtin_elementwise_max(am, __builtin_bit_cast(u16x2, v[j][c].x & 0x7FFF7FFFu));
+      am = __builtin_elementwise_max(am, __builtin_bit_cast(u16x2, v[j][c].y & 0x7FFF7FFFu));
+      am = __builtin_elementwise_max(am, __builtin_bit_cast(u16x2, v[j][c].z & 0x7FFF7FFFu));
+      am = __builtin_elementwise_max(am, __builtin_bit_cast(u16x2, v[j][c].w & 0x7FFF7FFFu));
+    }
+  }
+  uint32_t amax = am.x > am.y ? am.x : am.y;
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    const uint32_t o = static_cast<uint32_t>(__shfl_xor(static_cast<int>(amax), off, 64));
+    amax = amax > o ? amax : o;
+  }
+  if (nwaves > 1) {
+    if (lane == 0) wave_max[wave] = amax;
+    __syncthreads();
+    amax = wave_max[0];
+    for (int w = 1; w < nwaves; ++w) amax = amax > wave_max[w] ? amax : wave_max[w];
+  }
+  // Non-negative floats order like their bit patterns.
+  const float a = __uint_as_float(amax << 16);
+  const float s = a / 7.0f;
+  if (live && threadIdx.x == 0) scale[row] = s;
+  const float rcp = (s == 0.0f) ? 0.0f : 1.0f / s;
+  const bool exact_row = __builtin_isinf(rcp);
+
+#pragma unroll
+  for (int j = 0; j < NJ; ++j) {
+    const int gi = threadIdx.x + T * j;
+    if (gi >= groups) continue;
+    float q[32];
+    if (s == 0.0f) {
+#pragma unroll
+      for (int p = 0; p < 32; ++p) q[p] = 0.0f;
+    } else {
+      const uint32_t w[16] = {v[j][0].x, v[j][0].y, v[j][0].z, v[j][0].w, v[j][1].x, v[j][1].y,
+                              v[j][1].z, v[j][1].w, v[j][2].x, v[j][2].y, v[j][2].z, v[j][2].w,
+                              v[j][3].x, v[j][3].y, v[j][3].z, v[j][3].w};
+      codes32(w, s, rcp, exact_row, q);
+    }
+    store_group(out, ksteps, row, gi, bf6_group(q));
+  }
+}
+
+// Canonical packed int4 codes -> BF6 operand.  One thread per (row, 32-code
+// group) of the padded operand; padding rows and codes are written as zeros.
+__global__ __launch_bounds__(256) void int4_to_f6_kernel(const uint8_t* __restrict__ q, int64_t rows,
+                                                         int64_t rows_padded, int64_t K, int64_t ksteps,
+                                                         uint8_t* __restrict__ out) {
+  const int groups = static_cast<int>(2 * ksteps);
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (i >= rows_padded * groups) return;
+  const int64_t row = i / groups;
+  const int gi = static_cast<int>(i % groups);
+  uint4 p = make_uint4(0, 0, 0, 0);
+  if (row < rows && 32 * static_cast<int64_t>(gi) < K)
+    p = *reinterpret_cast<const uint4*>(q + row * (K / 2) + 16 * static_cast<int64_t>(gi));
+  const uint32_t w[4] = {p.x, p.y, p.z, p.w};
+  float c[32];
+#pragma unroll
+  for (int d = 0; d < 4; ++d)
+#pragma unroll
+    for (int n = 0; n < 8; ++n)  // nibble n of dword d is code 8d + n (even codes in low nibbles)
+      c[8 * d + n] = static_cast<float>(static_cast<int>(w[d] << (28 - 4 * n)) >> 28);
+  store_group(out, ksteps, row, gi, bf6_group(c));
+}
+
+// ---------------------------------------------------------------------------
+// GEMM
+
+typedef int v4i32 __attribute__((ext_vector_type(4)));
+typedef int v2i32 __attribute__((ext_vector_type(2)));
+typedef v4i32 v4i32_a8 __attribute__((aligned(8)));
+
+struct WFrag {
+  v8i f[2][2];  // [k-step][band]; dwords 0..5 used
+};
+
+__device__ __forceinline__ v8i join(v4i32 a, v2i32 b) { return v8i{a.x, a.y, a.z, a.w, b.x, b.y, 0, 0}; }
+__device__ __forceinline__ v8i join(v4i32 a, v4i32 b) { return v8i{a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w}; }
+
+constexpr int kWaitcntBase = (0x7 << 4) | (0xF << 8);  // expcnt, lgkmcnt: no wait
+constexpr int vmcnt_imm(int n) { return kWaitcntBase | (n & 0xF) | ((n >> 4) << 14); }
+constexpr int kLgkm0 = 0xC07F;                          // lgkmcnt(0), vmcnt and expcnt: no wait
+constexpr int kWLoads = 8;                              // weight loads per wave per stage
+
+template <Epilogue EPI, bool HAS_BIAS>
+__global__ __launch_bounds__(kF6Threads, 1) void w4a4_f6_gemm_kernel(
+    const uint8_t* __restrict__ xf6, const float* __restrict__ sx, int M, int mbands,
+    const uint8_t* __restrict__ wf6, const float* __restrict__ sw, int N, int nbands, int ksteps,
+    const uint16_t* __restrict__ bias, void* __restrict__ out, int tiles_m, int tiles_n) {
+  // The 72 KiB ring as three separate arrays (each with 16 bytes read, and
+  // ignored, past its last fragment's 8-byte parts).  With the stage loop
+  // unrolled by six every slot is known at compile time, so the compiler
+  // can tell the slot being read from the one the DMA is writing.
+  __shared__ uint4 lds0[kStageU4 + 1];
+  __shared__ uint4 lds1[kStageU4 + 1];
+  __shared__ uint4 lds2[kStageU4 + 1];
+  auto slot = [&](int k) -> uint4* { return k == 0 ? lds0 : (k == 1 ? lds1 : lds2); };
+
+  TileCoord tc;
+  if (!tile_of_block(blockIdx.x, tiles_m, tiles_n, &tc)) return;
+  const int m0 = tc.tm * kFBM;
+  const int n0 = tc.tn * kFBN;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave >> 2, wn = wave & 3;  // activation half (4 bands), weight quarter (2 bands)
+  const int T = ksteps / 2;                  // stages of 128 codes
+  const int last = T - 1;
+
+  const __amdgpu_buffer_rsrc_t rsx = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint8_t*>(xf6), 0, static_cast<int>(static_cast<int64_t>(mbands) * ksteps * kFragBytes),
+      kBufferFlags);
+  const __amdgpu_buffer_rsrc_t rsw = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint8_t*>(wf6), 0, static_cast<int>(static_cast<int64_t>(nbands) * ksteps * kFragBytes),
+      kBufferFlags);
+
+  // Activation DMA: the 16 fragments of a stage ((k-step s, band b) in order
+  // 8s + b) are contiguous 1536-byte blocks in LDS; slot part
+  // Q = 64 (3 wave + j) + lane of the stage is byte 16 (Q % 96) of fragment
+  // Q / 96.  Bands past the operand are clamped (their results are discarded).
+  uint32_t od[kDmaPerWave];
+#pragma unroll
+  for (int j = 0; j < kDmaPerWave; ++j) {
+    const int Q = 64 * (kDmaPerWave * wave + j) + lane;
+    const int R = Q / 96, q = Q % 96;
+    const int s = R >> 3, band = min(m0 / 32 + (R & 7), mbands - 1);
+    od[j] = (static_cast<uint32_t>(band) * static_cast<uint32_t>(ksteps) + s) * kFragBytes + 16 * q;
+  }
+  // Weight bands of this wave (clamped likewise).
+  uint32_t wb[2];
+#pragma unroll
+  for (int f = 0; f < 2; ++f)
+    wb[f] = static_cast<uint32_t>(min(n0 / 32 + 2 * wn + f, nbands - 1)) * static_cast<uint32_t>(ksteps) *
+            kFragBytes;
+
+  // DMA of stage t's activations into slot k.
+  auto issue_dma = [&](int t, int k) {
+    uint4* dst = slot(k) + 64 * kDmaPerWave * wave;
+#pragma unroll
+    for (int j = 0; j < kDmaPerWave; ++j) dma16(rsx, dst + 64 * j, od[j], 2 * kFragBytes * t);
+  };
+  auto load_w = [&](WFrag& w, int t) {
+#pragma unroll
+    for (int s = 0; s < 2; ++s)
+#pragma unroll
+      for (int f = 0; f < 2; ++f) {
+        const int so = (2 * t + s) * kFragBytes;
+        const v4i32 a = __builtin_bit_cast(v4i32, __builtin_amdgcn_raw_buffer_load_b128(rsw, wb[f] + 16 * lane, so, 0));
+        const v2i32 b = __builtin_bit_cast(v2i32, __builtin_amdgcn_raw_buffer_load_b64(rsw, wb[f] + 1024 + 8 * lane, so, 0));
+        w.f[s][f] = join(a, b);
+      }
+  };
+  // B fragment (k-step s, band 4 wm + fm) from slot k: the 16-byte part and
+  // the 8-byte part, the latter read as 16 bytes whose upper half is unused.
+  auto read_b = [&](int k, int s, int fm) {
+    const uint8_t* p = reinterpret_cast<const uint8_t*>(slot(k)) + (s * 8 + 4 * wm + fm) * kFragBytes;
+    return join(*reinterpret_cast<const v4i32*>(p + 16 * lane),
+                *reinterpret_cast<const v4i32_a8*>(p + 1024 + 8 * lane));
+  };
+
+  v16f acc[2][4];
+#pragma unroll
+  for (int f = 0; f < 2; ++f)
+#pragma unroll
+    for (int fm = 0; fm < 4; ++fm) acc[f][fm] = v16f{};
+
+  // Prologue: weights of stage 0, activations of stages 0..2.  Loads for
+  // stages past the last one are issued anyway, for the last stage again
+  // (every address stays inside the operands): the weights land in a register
+  // set that is not used again and the activations in a slot whose data is
+  // not read, which keeps the wait counts below constant.
+  WFrag w0, w1;
+  load_w(w0, 0);
+  issue_dma(0, 0);
+  issue_dma(min(1, last), 1);
+  issue_dma(min(2, last), 2);
+  __builtin_amdgcn_s_waitcnt(vmcnt_imm(2 * kDmaPerWave));  // DMA(0)
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_sched_barrier(0);
+  // A wave's activation fragments of a stage, (k-step s, band fm) in order
+  // 4s + fm, roll through a window of four: fragment i is read while the
+  // MFMAs of fragment i - 4 run.
+  v8i bq0 = read_b(0, 0, 0), bq1 = read_b(0, 0, 1), bq2 = read_b(0, 0, 2), bq3 = read_b(0, 0, 3);
+
+  // One stage t = t0 + I, t0 a multiple of 6: slot I % 3 and weight set
+  // I % 2, both known at compile time.  The stage starts by loading stage
+  // t + 1's weights into the other set (done with at stage t - 1).  Half way
+  // through, once every wave has read the whole slot (lgkmcnt(0) + barrier)
+  // and DMA(t + 1) has landed, the slot takes the DMA of stage t + 3.  The
+  // wait there, vmcnt(11), leaves in flight exactly the loads issued since
+  // stage t's weights: DMA(t + 2) and stage t + 1's weights.
+  WFrag* wset[2] = {&w0, &w1};
+  auto stage = [&](int t, auto I) {
+    constexpr int i = decltype(I)::value;
+    constexpr int cur = i % 3, nxt = (i + 1) % 3;
+    const WFrag& wc = *wset[i % 2];
+    load_w(*wset[(i + 1) % 2], min(t + 1, last));
+#define JQ_F6_STEP(S, FM, BQ, NK, NS, NFM)                                                            \
+  acc[0][FM] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(wc.f[S][0], BQ, acc[0][FM], 3, 3, 0, 127, \
+                                                                0, 127);                              \
+  acc[1][FM] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(wc.f[S][1], BQ, acc[1][FM], 3, 3, 0, 127, \
+                                                                0, 127);                              \
+  BQ = read_b(NK, NS, NFM);
+    // k-step 0; the window moves on to k-step 1 of this stage
+    JQ_F6_STEP(0, 0, bq0, cur, 1, 0)
+    JQ_F6_STEP(0, 1, bq1, cur, 1, 1)
+    JQ_F6_STEP(0, 2, bq2, cur, 1, 2)
+    JQ_F6_STEP(0, 3, bq3, cur, 1, 3)
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_waitcnt(kLgkm0);
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(kWLoads + kDmaPerWave));
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+    issue_dma(min(t + 3, last), cur);
+    // k-step 1; the window moves on to k-step 0 of the next stage (past the
+    // last stage these reads are of a slot whose data is not used)
+    JQ_F6_STEP(1, 0, bq0, nxt, 0, 0)
+    JQ_F6_STEP(1, 1, bq1, nxt, 0, 1)
+    JQ_F6_STEP(1, 2, bq2, nxt, 0, 2)
+    JQ_F6_STEP(1, 3, bq3, nxt, 0, 3)
+#undef JQ_F6_STEP
+    __builtin_amdgcn_sched_barrier(0);
+  };
+  for (int t = 0; t < T; t += 6) {
+    stage(t, std::integral_constant<int, 0>{});
+#define JQ_F6_NEXT(N) \
+    if (t + N < T) stage(t + N, std::integral_constant<int, N>{});
+    JQ_F6_NEXT(1) JQ_F6_NEXT(2) JQ_F6_NEXT(3) JQ_F6_NEXT(4) JQ_F6_NEXT(5)
+#undef JQ_F6_NEXT
+  }
+  // no load may still be writing LDS or registers when the wave ends
+  __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+
+  // Epilogue: lane holds column m = m0 + 128 wm + 32 fm + (lane & 31) and
+  // rows n = n0 + 64 wn + 32 f + 8 j + 4 (lane >> 5) + r of y^T.
+  const int mb = m0 + 128 * wm + (lane & 31);
+  const int nb = n0 + 64 * wn + 4 * (lane >> 5);
+  const bool full = (m0 + kFBM <= M) && (n0 + kFBN <= N) && (N % 4 == 0);
+  if constexpr (EPI == Epilogue::kInt32) {
+    int32_t* o = static_cast<int32_t*>(out);
+#pragma unroll
+    for (int f = 0; f < 2; ++f)
+#pragma unroll
+      for (int fm = 0; fm < 4; ++fm) {
+        const int m = mb + 32 * fm;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int n = nb + 32 * f + 8 * j;
+          const int v0 = static_cast<int>(acc[f][fm][4 * j]), v1 = static_cast<int>(acc[f][fm][4 * j + 1]);
+          const int v2 = static_cast<int>(acc[f][fm][4 * j + 2]), v3 = static_cast<int>(acc[f][fm][4 * j + 3]);
+          int32_t* p = o + static_cast<int64_t>(m) * N + n;
+          if (full) {
+            *reinterpret_cast<int4*>(p) = make_int4(v0, v1, v2, v3);
+          } else if (m < M) {
+            if (n + 0 < N) p[0] = v0;
+            if (n + 1 < N) p[1] = v1;
+            if (n + 2 < N) p[2] = v2;
+            if (n + 3 < N) p[3] = v3;
+          }
+        }
+      }
+  } else {
+    uint16_t* o = static_cast<uint16_t*>(out);
+    float sxv[4];
+#pragma unroll
+    for (int fm = 0; fm < 4; ++fm) sxv[fm] = sx[min(mb + 32 * fm, M - 1)];
+#pragma unroll
+    for (int f = 0; f < 2; ++f)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int n = nb + 32 * f + 8 * j;
+        float swv[4], bv[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int nn = min(n + r, N - 1);
+          swv[r] = sw[nn];
+          bv[r] = HAS_BIAS ? __uint_as_float(static_cast<uint32_t>(bias[nn]) << 16) : 0.0f;
+        }
+#pragma unroll
+        for (int fm = 0; fm < 4; ++fm) {
+          const int m = mb + 32 * fm;
+          uint16_t h[4];
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            float v = acc[f][fm][4 * j + r];
+            v = v * sxv[fm];
+            v = v * swv[r];
+            if (HAS_BIAS) v = v + bv[r];
+            h[r] = __builtin_bit_cast(uint16_t, static_cast<__bf16>(v));
+          }
+          uint16_t* p = o + static_cast<int64_t>(m) * N + n;
+          if (full) {
+            *reinterpret_cast<uint2*>(p) = make_uint2(h[0] | (static_cast<uint32_t>(h[1]) << 16),
+                                                      h[2] | (static_cast<uint32_t>(h[3]) << 16));
+          } else if (m < M) {
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+              if (n + r < N) p[r] = h[r];
+          }
+        }
+      }
+  }
+}
+
+template <int NJ>
+hipError_t launch_qf6(const uint16_t* x, int64_t M, int64_t K, int64_t ksteps, uint8_t* out, float* s, int threads,
+                      hipStream_t st) {
+  const int64_t rows_padded = (M + 31) / 32 * 32;
+  const int64_t groups_of_8_bands = (rows_padded / 32 + kNumXcd - 1) / kNumXcd;
+  const dim3 grid(static_cast<unsigned>(groups_of_8_bands * 32 * kNumXcd));
+  hipLaunchKernelGGL(quantize_rows_f6_kernel<NJ>, grid, dim3(threads), 0, st, x, M, K, rows_padded, ksteps, out, s);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+int64_t f6_ksteps(int64_t K) { return (K + 127) / 128 * 2; }
+
+int64_t f6_operand_bytes(int64_t rows, int64_t K) { return (rows + 31) / 32 * f6_ksteps(K) * kFragBytes; }
+
+hipError_t launch_quantize_rows_f6(const uint16_t* x, int64_t M, int64_t K, uint8_t* out, float* scale,
+                                   hipStream_t st) {
+  const int64_t ksteps = f6_ksteps(K);
+  const int64_t groups = 2 * ksteps;
+  // Up to 512 threads per row, each holding NJ groups of 32 codes.
+  const int64_t threads = groups <= 512 ? (groups + 63) / 64 * 64 : 512;
+  const int64_t nj = (groups + threads - 1) / threads;
+  const int th = static_cast<int>(threads);
+  if (nj <= 1) return launch_qf6<1>(x, M, K, ksteps, out, scale, th, st);
+  if (nj <= 2) return launch_qf6<2>(x, M, K, ksteps, out, scale, th, st);
+  return launch_qf6<4>(x, M, K, ksteps, out, scale, th, st);
+}
+
+hipError_t launch_int4_to_f6(const uint8_t* q, int64_t rows, int64_t K, uint8_t* out, hipStream_t st) {
+  const int64_t ksteps = f6_ksteps(K);
+  const int64_t rows_padded = (rows + 31) / 32 * 32;
+  const int64_t total = rows_padded * 2 * ksteps;
+  const dim3 grid(static_cast<unsigned>((total + 255) / 256));
+  hipLaunchKernelGGL(int4_to_f6_kernel, grid, dim3(256), 0, st, q, rows, rows_padded, K, ksteps, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_w4a4_f6_gemm(Epilogue epi, const uint8_t* xf6, const float* sx, int64_t M, int64_t K,
+                               const uint8_t* wf6, const float* sw, int64_t N, const uint16_t* bias, void* out,
+                               hipStream_t st) {
+  const int tiles_m = static_cast<int>((M + kFBM - 1) / kFBM);
+  const int tiles_n = static_cast<int>((N + kFBN - 1) / kFBN);
+  const int64_t T = static_cast<int64_t>(tiles_m) * tiles_n;
+  const int64_t per_xcd = (T + kNumXcd - 1) / kNumXcd;
+  const dim3 grid(static_cast<unsigned>(per_xcd * kNumXcd));
+  const int ksteps = static_cast<int>(f6_ksteps(K));
+  const int mbands = static_cast<int>((M + 31) / 32);
+  const int nbands = static_cast<int>((N + 31) / 32);
+  const int Mi = static_cast<int>(M), Ni = static_cast<int>(N);
+#define JQ_F6(E, B)                                                                                              \
+  hipLaunchKernelGGL((w4a4_f6_gemm_kernel<E, B>), grid, dim3(kF6Threads), 0, st, xf6, sx, Mi, mbands, wf6, sw, Ni, \
+                     nbands, ksteps, bias, out, tiles_m, tiles_n)
+  if (epi == Epilogue::kInt32) JQ_F6(Epilogue::kInt32, false);
+  else if (bias != nullptr) JQ_F6(Epilogue::kBf16, true);
+  else JQ_F6(Epilogue::kBf16, false);
+#undef JQ_F6
+  return hipGetLastError();
+}
+
+}  // namespace jq

@@ -283,3 +283,106 @@ jq_status jq_w4a4g_gemm_f32(const void* q_packed, const float* scales, int64_t M
 }
 
 }  // extern "C"
+
+// ---------------------------------------------------------------------------
+// BF6 engine: the same layer on the 6-bit matrix cores
+
+namespace {
+
+jq_status check_f6_operands(int64_t M, int64_t N, int64_t K) {
+  jq_status st = check_shape(M, K);
+  if (st != JQ_OK) return st;
+  st = check_shape(N, K);
+  if (st != JQ_OK) return st;
+  // 32-bit tile indices; 31-bit buffer descriptors over both operands.
+  if (((M + 255) / 256) * ((N + 255) / 256) > (int64_t(1) << 26)) return JQ_ERR_UNSUPPORTED_SHAPE;
+  if (jq::f6_operand_bytes(M, K) >= (int64_t(1) << 31) || jq::f6_operand_bytes(N, K) >= (int64_t(1) << 31))
+    return JQ_ERR_UNSUPPORTED_SHAPE;
+  return JQ_OK;
+}
+
+jq_status check_f6_gemm(const void* xf6, const float* sx, int64_t M, int64_t K, const void* wf6, const float* sw,
+                        int64_t N, const void* bias, const void* y, bool need_scales) {
+  if (xf6 == nullptr || wf6 == nullptr || y == nullptr) return JQ_ERR_INVALID_ARG;
+  if (need_scales && (sx == nullptr || sw == nullptr)) return JQ_ERR_INVALID_ARG;
+  const jq_status st = check_f6_operands(M, N, K);
+  if (st != JQ_OK) return st;
+  if (!aligned(xf6, 16) || !aligned(wf6, 16) || !aligned(y, 16)) return JQ_ERR_MISALIGNED;
+  if ((sx != nullptr && !aligned(sx, 4)) || (sw != nullptr && !aligned(sw, 4))) return JQ_ERR_MISALIGNED;
+  if (bias != nullptr && !aligned(bias, 2)) return JQ_ERR_MISALIGNED;
+  return JQ_OK;
+}
+
+size_t f6_workspace_bytes(int64_t M, int64_t K) {
+  if (check_shape(M, K) != JQ_OK) return 0;
+  return round_up(static_cast<size_t>(jq::f6_operand_bytes(M, K)), kWsAlign) +
+         round_up(static_cast<size_t>(M) * sizeof(float), kWsAlign);
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t jq_f6_operand_bytes(int64_t rows, int64_t K) {
+  if (check_shape(rows, K) != JQ_OK) return 0;
+  return static_cast<size_t>(jq::f6_operand_bytes(rows, K));
+}
+
+jq_status jq_quantize_act_f6(const void* x_bf16, int64_t M, int64_t K, void* xf6, float* scale, void* stream) {
+  if (x_bf16 == nullptr || xf6 == nullptr || scale == nullptr) return JQ_ERR_INVALID_ARG;
+  const jq_status st = check_shape(M, K);
+  if (st != JQ_OK) return st;
+  if (!aligned(x_bf16, 16) || !aligned(xf6, 16) || !aligned(scale, 4)) return JQ_ERR_MISALIGNED;
+  return from_hip(jq::launch_quantize_rows_f6(static_cast<const uint16_t*>(x_bf16), M, K,
+                                              static_cast<uint8_t*>(xf6), scale, as_stream(stream)));
+}
+
+jq_status jq_int4_to_f6(const void* q_packed, int64_t rows, int64_t K, void* f6, void* stream) {
+  if (q_packed == nullptr || f6 == nullptr) return JQ_ERR_INVALID_ARG;
+  const jq_status st = check_shape(rows, K);
+  if (st != JQ_OK) return st;
+  if (!aligned(q_packed, 16) || !aligned(f6, 16)) return JQ_ERR_MISALIGNED;
+  return from_hip(jq::launch_int4_to_f6(static_cast<const uint8_t*>(q_packed), rows, K, static_cast<uint8_t*>(f6),
+                                        as_stream(stream)));
+}
+
+size_t jq_w4a4_f6_workspace_bytes(int64_t M, int64_t K) { return f6_workspace_bytes(M, K); }
+
+jq_status jq_w4a4_f6_linear(const void* x_bf16, int64_t M, int64_t K, const void* wf6, const float* w_scale,
+                            int64_t N, const void* bias_bf16, void* y_bf16, void* workspace,
+                            size_t workspace_bytes, void* stream) {
+  if (x_bf16 == nullptr || workspace == nullptr) return JQ_ERR_INVALID_ARG;
+  // the activation operand lives in the workspace; check the rest with stand-ins
+  const jq_status st = check_f6_gemm(x_bf16, w_scale, M, K, wf6, w_scale, N, bias_bf16, y_bf16, true);
+  if (st != JQ_OK) return st;
+  if (!aligned(workspace, kWsAlign)) return JQ_ERR_MISALIGNED;
+  if (workspace_bytes < f6_workspace_bytes(M, K)) return JQ_ERR_WORKSPACE_TOO_SMALL;
+  uint8_t* xf6 = static_cast<uint8_t*>(workspace);
+  float* sx = reinterpret_cast<float*>(xf6 + round_up(static_cast<size_t>(jq::f6_operand_bytes(M, K)), kWsAlign));
+  hipError_t e = jq::launch_quantize_rows_f6(static_cast<const uint16_t*>(x_bf16), M, K, xf6, sx,
+                                             as_stream(stream));
+  if (e != hipSuccess) return JQ_ERR_HIP;
+  e = jq::launch_w4a4_f6_gemm(jq::Epilogue::kBf16, xf6, sx, M, K, static_cast<const uint8_t*>(wf6), w_scale, N,
+                              static_cast<const uint16_t*>(bias_bf16), y_bf16, as_stream(stream));
+  return from_hip(e);
+}
+
+jq_status jq_w4a4_f6_gemm(const void* xf6, const float* scale, int64_t M, int64_t K, const void* wf6,
+                          const float* w_scale, int64_t N, const void* bias_bf16, void* y_bf16, void* stream) {
+  const jq_status st = check_f6_gemm(xf6, scale, M, K, wf6, w_scale, N, bias_bf16, y_bf16, true);
+  if (st != JQ_OK) return st;
+  return from_hip(jq::launch_w4a4_f6_gemm(jq::Epilogue::kBf16, static_cast<const uint8_t*>(xf6), scale, M, K,
+                                          static_cast<const uint8_t*>(wf6), w_scale, N,
+                                          static_cast<const uint16_t*>(bias_bf16), y_bf16, as_stream(stream)));
+}
+
+jq_status jq_w4a4_f6_gemm_i32(const void* xf6, int64_t M, int64_t K, const void* wf6, int64_t N, int32_t* acc,
+                              void* stream) {
+  const jq_status st = check_f6_gemm(xf6, nullptr, M, K, wf6, nullptr, N, nullptr, acc, false);
+  if (st != JQ_OK) return st;
+  return from_hip(jq::launch_w4a4_f6_gemm(jq::Epilogue::kInt32, static_cast<const uint8_t*>(xf6), nullptr, M, K,
+                                          static_cast<const uint8_t*>(wf6), nullptr, N, nullptr, acc,
+                                          as_stream(stream)));
+}
+
+}  // extern "C"

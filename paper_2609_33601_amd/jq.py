@@ -40,6 +40,13 @@ SIGNATURES = {
     "jq_w4a4g_linear": (ctypes.c_int, [_vp, _i64, _i64, _i64, _vp, _fp, _i64, _vp, _vp, _vp, _sz, _vp]),
     "jq_w4a4g_gemm": (ctypes.c_int, [_vp, _fp, _i64, _i64, _i64, _vp, _fp, _i64, _vp, _vp, _vp]),
     "jq_w4a4g_gemm_f32": (ctypes.c_int, [_vp, _fp, _i64, _i64, _i64, _vp, _fp, _i64, _fp, _vp]),
+    "jq_f6_operand_bytes": (_sz, [_i64, _i64]),
+    "jq_quantize_act_f6": (ctypes.c_int, [_vp, _i64, _i64, _vp, _fp, _vp]),
+    "jq_int4_to_f6": (ctypes.c_int, [_vp, _i64, _i64, _vp, _vp]),
+    "jq_w4a4_f6_workspace_bytes": (_sz, [_i64, _i64]),
+    "jq_w4a4_f6_linear": (ctypes.c_int, [_vp, _i64, _i64, _vp, _fp, _i64, _vp, _vp, _vp, _sz, _vp]),
+    "jq_w4a4_f6_gemm": (ctypes.c_int, [_vp, _fp, _i64, _i64, _vp, _fp, _i64, _vp, _vp, _vp]),
+    "jq_w4a4_f6_gemm_i32": (ctypes.c_int, [_vp, _i64, _i64, _vp, _i64, _ip, _vp]),
 }
 
 _lib = None
@@ -351,6 +358,96 @@ def jq_w4a4g_gemm_f32(q, scale, wq, w_scale, G, out=None, stream=None):
                                  _dev(out, torch.float32, (M, N), "out"), _stream_ptr(stream))
     _check(st, "jq_w4a4g_gemm_f32")
     return out
+
+
+# ---------------------------------------------------------------------------
+# BF6 engine: the same layer on the 6-bit matrix cores (operands in the BF6
+# layout of include/jq.h, held as flat uint8 tensors)
+# ---------------------------------------------------------------------------
+
+
+def jq_f6_operand_bytes(rows, K):
+    return int(lib().jq_f6_operand_bytes(int(rows), int(K)))
+
+
+def jq_w4a4_f6_workspace_bytes(M, K):
+    return int(lib().jq_w4a4_f6_workspace_bytes(int(M), int(K)))
+
+
+def jq_quantize_act_f6(x, xf6=None, scale=None, stream=None):
+    """x bf16 [M,K] -> (BF6 activation operand uint8 [jq_f6_operand_bytes(M,K)], scale fp32 [M])."""
+    torch = _torch()
+    M, K = x.shape
+    nb = jq_f6_operand_bytes(M, K)
+    if xf6 is None:
+        xf6 = torch.empty((nb,), dtype=torch.uint8, device=x.device)
+    if scale is None:
+        scale = torch.empty((M,), dtype=torch.float32, device=x.device)
+    st = lib().jq_quantize_act_f6(_dev(x, torch.bfloat16, None, "x"), M, K, _dev(xf6, torch.uint8, (nb,), "xf6"),
+                                  _dev(scale, torch.float32, (M,), "scale"), _stream_ptr(stream))
+    _check(st, "jq_quantize_act_f6")
+    return xf6, scale
+
+
+def jq_int4_to_f6(q, out=None, stream=None):
+    """Packed int4 codes uint8 [rows,K/2] -> BF6 operand uint8 [jq_f6_operand_bytes(rows,K)]."""
+    torch = _torch()
+    rows, Kh = q.shape
+    nb = jq_f6_operand_bytes(rows, 2 * Kh)
+    if out is None:
+        out = torch.empty((nb,), dtype=torch.uint8, device=q.device)
+    st = lib().jq_int4_to_f6(_dev(q, torch.uint8, (rows, Kh), "q"), rows, 2 * Kh,
+                             _dev(out, torch.uint8, (nb,), "out"), _stream_ptr(stream))
+    _check(st, "jq_int4_to_f6")
+    return out
+
+
+def jq_w4a4_f6_linear(x, wf6, w_scale, bias=None, y=None, workspace=None, stream=None):
+    """y = W4A4 linear of x (bf16 [M,K]) on the BF6 engine; returns bf16 [M,N]."""
+    torch = _torch()
+    M, K = x.shape
+    N = w_scale.shape[0]
+    if y is None:
+        y = torch.empty((M, N), dtype=torch.bfloat16, device=x.device)
+    if workspace is None:
+        workspace = torch.empty((jq_w4a4_f6_workspace_bytes(M, K),), dtype=torch.uint8, device=x.device)
+    bptr = ctypes.c_void_p(None) if bias is None else _dev(bias, torch.bfloat16, (N,), "bias")
+    st = lib().jq_w4a4_f6_linear(_dev(x, torch.bfloat16, None, "x"), M, K,
+                                 _dev(wf6, torch.uint8, (jq_f6_operand_bytes(N, K),), "wf6"),
+                                 _dev(w_scale, torch.float32, (N,), "w_scale"), N, bptr,
+                                 _dev(y, torch.bfloat16, (M, N), "y"),
+                                 _dev(workspace, torch.uint8, None, "workspace"), workspace.numel(),
+                                 _stream_ptr(stream))
+    _check(st, "jq_w4a4_f6_linear")
+    return y
+
+
+def jq_w4a4_f6_gemm(xf6, scale, K, wf6, w_scale, bias=None, y=None, stream=None):
+    """GEMM + epilogue of the BF6 engine on a quantised activation operand; returns bf16 [M,N]."""
+    torch = _torch()
+    M, N = scale.shape[0], w_scale.shape[0]
+    if y is None:
+        y = torch.empty((M, N), dtype=torch.bfloat16, device=xf6.device)
+    bptr = ctypes.c_void_p(None) if bias is None else _dev(bias, torch.bfloat16, (N,), "bias")
+    st = lib().jq_w4a4_f6_gemm(_dev(xf6, torch.uint8, (jq_f6_operand_bytes(M, K),), "xf6"),
+                               _dev(scale, torch.float32, (M,), "scale"), M, K,
+                               _dev(wf6, torch.uint8, (jq_f6_operand_bytes(N, K),), "wf6"),
+                               _dev(w_scale, torch.float32, (N,), "w_scale"), N, bptr,
+                               _dev(y, torch.bfloat16, (M, N), "y"), _stream_ptr(stream))
+    _check(st, "jq_w4a4_f6_gemm")
+    return y
+
+
+def jq_w4a4_f6_gemm_i32(xf6, M, K, wf6, N, acc=None, stream=None):
+    """Exact accumulators int32 [M,N] of two BF6 operands."""
+    torch = _torch()
+    if acc is None:
+        acc = torch.empty((M, N), dtype=torch.int32, device=xf6.device)
+    st = lib().jq_w4a4_f6_gemm_i32(_dev(xf6, torch.uint8, (jq_f6_operand_bytes(M, K),), "xf6"), M, K,
+                                   _dev(wf6, torch.uint8, (jq_f6_operand_bytes(N, K),), "wf6"), N,
+                                   _dev(acc, torch.int32, (M, N), "acc"), _stream_ptr(stream))
+    _check(st, "jq_w4a4_f6_gemm_i32")
+    return acc
 
 
 # ---------------------------------------------------------------------------

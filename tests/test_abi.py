@@ -31,7 +31,7 @@ def header_functions():
 
 def test_exports_every_declared_symbol():
     names = header_functions()
-    assert len(names) == 18, names
+    assert len(names) == 25, names
     lib = ctypes.CDLL(jq.LIB_PATH)
     for n in names:
         assert hasattr(lib, n), f"libjq.so does not export {n}"
@@ -169,3 +169,55 @@ def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
     monkeypatch.setattr(jq, "LIB_PATH", str(tmp_path / "missing.so"))
     with pytest.raises(RuntimeError, match="missing"):
         jq.lib()
+
+
+# ---------------------------------------------------------------------------
+# BF6 engine
+
+
+def test_f6_sizes():
+    L = jq.lib()
+    # ceil(rows/32) bands x 2*ceil(K/128) k-steps x 1536 bytes
+    assert L.jq_f6_operand_bytes(9216, 12288) == 288 * 192 * 1536
+    assert L.jq_f6_operand_bytes(1, 64) == 1 * 2 * 1536
+    assert L.jq_f6_operand_bytes(33, 192) == 2 * 4 * 1536
+    assert L.jq_f6_operand_bytes(0, 64) == 0
+    assert L.jq_f6_operand_bytes(8, 96) == 0
+    assert L.jq_w4a4_f6_workspace_bytes(4608, 3072) == 144 * 48 * 1536 + 18432
+    assert L.jq_w4a4_f6_workspace_bytes(1, 64) == 3072 + 256
+    assert L.jq_w4a4_f6_workspace_bytes(5, 100) == 0
+
+
+def test_f6_quantize_and_convert_validation():
+    L = jq.lib()
+    assert L.jq_quantize_act_f6(None, 8, 64, A, A, None) == jq.JQ_ERR_INVALID_ARG
+    assert L.jq_quantize_act_f6(A, 0, 64, A, A, None) == jq.JQ_ERR_INVALID_ARG
+    assert L.jq_quantize_act_f6(A, 8, 96, A, A, None) == jq.JQ_ERR_UNSUPPORTED_SHAPE
+    assert L.jq_quantize_act_f6(A, 8, 65600, A, A, None) == jq.JQ_ERR_UNSUPPORTED_SHAPE
+    assert L.jq_quantize_act_f6(MIS, 8, 64, A, A, None) == jq.JQ_ERR_MISALIGNED
+    assert L.jq_quantize_act_f6(A, 8, 64, MIS, A, None) == jq.JQ_ERR_MISALIGNED
+    assert L.jq_int4_to_f6(None, 8, 64, A, None) == jq.JQ_ERR_INVALID_ARG
+    assert L.jq_int4_to_f6(A, 8, 64, None, None) == jq.JQ_ERR_INVALID_ARG
+    assert L.jq_int4_to_f6(A, -1, 64, A, None) == jq.JQ_ERR_INVALID_ARG
+    assert L.jq_int4_to_f6(A, 8, 32, A, None) == jq.JQ_ERR_UNSUPPORTED_SHAPE
+    assert L.jq_int4_to_f6(A, 8, 64, MIS, None) == jq.JQ_ERR_MISALIGNED
+
+
+def test_f6_gemm_and_linear_validation():
+    L = jq.lib()
+    ws = L.jq_w4a4_f6_workspace_bytes(8, 64)
+    assert L.jq_w4a4_f6_linear(None, 8, 64, A, A, 8, None, A, A, ws, None) == jq.JQ_ERR_INVALID_ARG
+    assert L.jq_w4a4_f6_linear(A, 8, 64, A, A, 8, None, A, None, ws, None) == jq.JQ_ERR_INVALID_ARG
+    assert L.jq_w4a4_f6_linear(A, 8, 64, A, A, 8, None, A, A, ws - 1, None) == jq.JQ_ERR_WORKSPACE_TOO_SMALL
+    assert L.jq_w4a4_f6_linear(A, 8, 64, A, A, 8, None, A, A + 16, ws, None) == jq.JQ_ERR_MISALIGNED
+    assert L.jq_w4a4_f6_linear(A, 8, 64, MIS, A, 8, None, A, A, ws, None) == jq.JQ_ERR_MISALIGNED
+    assert L.jq_w4a4_f6_linear(A, 8, 64, A, A, 8, A + 1, A, A, ws, None) == jq.JQ_ERR_MISALIGNED
+    assert L.jq_w4a4_f6_gemm(A, None, 8, 64, A, A, 8, None, A, None) == jq.JQ_ERR_INVALID_ARG
+    assert L.jq_w4a4_f6_gemm(A, A, 8, 160, A, A, 8, None, A, None) == jq.JQ_ERR_UNSUPPORTED_SHAPE
+    assert L.jq_w4a4_f6_gemm(A, A, 8, 64, A, A, 0, None, A, None) == jq.JQ_ERR_INVALID_ARG
+    assert L.jq_w4a4_f6_gemm(A, A, 8, 64, A, A, 8, None, MIS, None) == jq.JQ_ERR_MISALIGNED
+    assert L.jq_w4a4_f6_gemm_i32(None, 8, 64, A, 8, A, None) == jq.JQ_ERR_INVALID_ARG
+    assert L.jq_w4a4_f6_gemm_i32(A, 8, 64, A, 8, None, None) == jq.JQ_ERR_INVALID_ARG
+    assert L.jq_w4a4_f6_gemm_i32(A, 8, 64, A, 8, MIS, None) == jq.JQ_ERR_MISALIGNED
+    # operands of 2 GiB or more are refused (31-bit buffer descriptors)
+    assert L.jq_w4a4_f6_gemm_i32(A, 1 << 22, 65536, A, 8, A, None) == jq.JQ_ERR_UNSUPPORTED_SHAPE
