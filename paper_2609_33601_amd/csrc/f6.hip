@@ -40,10 +40,7 @@
 //   * Activations: shared by the four waves, staged through LDS.  A stage is
 //     128 codes of K (two k-steps x eight bands = 16 fragments, 24 KiB), moved
 //     from global memory by buffer_load ... lds (no registers) into a ring of
-//     four stage slots, three stages ahead.  The 8-byte part of a fragment
-//     lane is read from LDS as 16 bytes (the upper half is ignored by the
-//     6-bit MFMA), so that no two fragments' reads can be fused into one
-//     instruction whose result would then have to be copied apart.
+//     three stage slots, three stages ahead.
 //   * Weights: private to a wave, loaded straight into registers two stages
 //     ahead (a ring of three register sets, so the stage loop is unrolled by 3).
 //   * Per stage: the sixteen activation fragments roll through a window of
@@ -60,6 +57,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <algorithm>
 #include <type_traits>
 
 #include "gemm_common.h"
@@ -248,14 +246,12 @@ __global__ __launch_bounds__(256) void int4_to_f6_kernel(const uint8_t* __restri
 
 typedef int v4i32 __attribute__((ext_vector_type(4)));
 typedef int v2i32 __attribute__((ext_vector_type(2)));
-typedef v4i32 v4i32_a8 __attribute__((aligned(8)));
 
 struct WFrag {
   v8i f[2][2];  // [k-step][band]; dwords 0..5 used
 };
 
 __device__ __forceinline__ v8i join(v4i32 a, v2i32 b) { return v8i{a.x, a.y, a.z, a.w, b.x, b.y, 0, 0}; }
-__device__ __forceinline__ v8i join(v4i32 a, v4i32 b) { return v8i{a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w}; }
 
 constexpr int kWaitcntBase = (0x7 << 4) | (0xF << 8);  // expcnt, lgkmcnt: no wait
 constexpr int vmcnt_imm(int n) { return kWaitcntBase | (n & 0xF) | ((n >> 4) << 14); }
@@ -266,26 +262,48 @@ template <Epilogue EPI, bool HAS_BIAS>
 __global__ __launch_bounds__(kF6Threads, 1) void w4a4_f6_gemm_kernel(
     const uint8_t* __restrict__ xf6, const float* __restrict__ sx, int M, int mbands,
     const uint8_t* __restrict__ wf6, const float* __restrict__ sw, int N, int nbands, int ksteps,
-    const uint16_t* __restrict__ bias, void* __restrict__ out, int tiles_m, int tiles_n) {
-  // The 72 KiB ring as three separate arrays (each with 16 bytes read, and
-  // ignored, past its last fragment's 8-byte parts).  With the stage loop
+    const uint16_t* __restrict__ bias, void* __restrict__ out, int tiles_m, int tiles_n, int grid_blocks) {
+  // The 72 KiB ring as three separate arrays.  With the stage loop
   // unrolled by six every slot is known at compile time, so the compiler
   // can tell the slot being read from the one the DMA is writing.
-  __shared__ uint4 lds0[kStageU4 + 1];
-  __shared__ uint4 lds1[kStageU4 + 1];
-  __shared__ uint4 lds2[kStageU4 + 1];
-  auto slot = [&](int k) -> uint4* { return k == 0 ? lds0 : (k == 1 ? lds1 : lds2); };
+  __shared__ uint4 lds0[kStageU4];
+  __shared__ uint4 lds1[kStageU4];
+  __shared__ uint4 lds2[kStageU4];
+  // Output staging for the epilogue: per wave 64 rows x 64 bf16 (128 bytes a
+  // row), 16-byte chunk c of row r at chunk c ^ ((r >> 1) & 7).
+  __shared__ uint4 stg[kF6Threads / 64][512];
+  // The current tile's scales and bias, moved in by DMA for the epilogue.
+  __shared__ float sc_x[kFBM];
+  __shared__ float sc_w[kFBN];
+  __shared__ uint32_t sc_b[kFBN / 2];
+  auto slot = [&](int k) __attribute__((always_inline)) { return k == 0 ? lds0 : (k == 1 ? lds1 : lds2); };
 
-  TileCoord tc;
-  if (!tile_of_block(blockIdx.x, tiles_m, tiles_n, &tc)) return;
-  const int m0 = tc.tm * kFBM;
-  const int n0 = tc.tn * kFBN;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave >> 2, wn = wave & 3;  // activation half (4 bands), weight quarter (2 bands)
-  const int T = ksteps / 2;                  // stages of 128 codes
+  const int T = ksteps / 2;                  // stages of 128 codes per tile
   const int last = T - 1;
+
+  // The block's tiles: virtual block ids v = blockIdx.x + i * grid_blocks of
+  // a grid of 8 * ceil(tiles / 8) blocks in the XCD-aware order (grid_blocks
+  // is a multiple of 8, so the XCD of every tile of this block is the
+  // block's own).  The launch makes every block walk a single tile when a
+  // tile has fewer than three stages, since the loads run three stages ahead
+  // and must not reach past the next tile.
+  int ntiles = 0;
+  {
+    const int vmax = (tiles_m * tiles_n + kNumXcd - 1) / kNumXcd * kNumXcd;
+    TileCoord tc;
+    for (int v = blockIdx.x; v < vmax && tile_of_block(v, tiles_m, tiles_n, &tc); v += grid_blocks) ++ntiles;
+  }
+  if (ntiles == 0) return;
+  auto tile_at = [&](int i, int* m0, int* n0) __attribute__((always_inline)) {
+    TileCoord tc;
+    tile_of_block(blockIdx.x + i * grid_blocks, tiles_m, tiles_n, &tc);
+    *m0 = tc.tm * kFBM;
+    *n0 = tc.tn * kFBN;
+  };
 
   const __amdgpu_buffer_rsrc_t rsx = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint8_t*>(xf6), 0, static_cast<int>(static_cast<int64_t>(mbands) * ksteps * kFragBytes),
@@ -297,45 +315,70 @@ __global__ __launch_bounds__(kF6Threads, 1) void w4a4_f6_gemm_kernel(
   // Activation DMA: the 16 fragments of a stage ((k-step s, band b) in order
   // 8s + b) are contiguous 1536-byte blocks in LDS; slot part
   // Q = 64 (3 wave + j) + lane of the stage is byte 16 (Q % 96) of fragment
-  // Q / 96.  Bands past the operand are clamped (their results are discarded).
-  uint32_t od[kDmaPerWave];
+  // Q / 96.  Per lane: the band within the tile and the byte offset within
+  // the band's stage.  Bands past the operand are clamped (their results are
+  // discarded).
+  int rband[kDmaPerWave];
+  uint32_t rpart[kDmaPerWave];
 #pragma unroll
   for (int j = 0; j < kDmaPerWave; ++j) {
     const int Q = 64 * (kDmaPerWave * wave + j) + lane;
     const int R = Q / 96, q = Q % 96;
-    const int s = R >> 3, band = min(m0 / 32 + (R & 7), mbands - 1);
-    od[j] = (static_cast<uint32_t>(band) * static_cast<uint32_t>(ksteps) + s) * kFragBytes + 16 * q;
+    rband[j] = R & 7;
+    rpart[j] = (R >> 3) * kFragBytes + 16 * q;
   }
-  // Weight bands of this wave (clamped likewise).
-  uint32_t wb[2];
-#pragma unroll
-  for (int f = 0; f < 2; ++f)
-    wb[f] = static_cast<uint32_t>(min(n0 / 32 + 2 * wn + f, nbands - 1)) * static_cast<uint32_t>(ksteps) *
-            kFragBytes;
+  const uint32_t band_bytes = static_cast<uint32_t>(ksteps) * kFragBytes;
 
-  // DMA of stage t's activations into slot k.
-  auto issue_dma = [&](int t, int k) {
+  // Stage `st` of the tile at (m0, n0): activations into slot k, weights into w.
+  auto issue_dma = [&](int m0, int st, int k) __attribute__((always_inline)) {
     uint4* dst = slot(k) + 64 * kDmaPerWave * wave;
 #pragma unroll
-    for (int j = 0; j < kDmaPerWave; ++j) dma16(rsx, dst + 64 * j, od[j], 2 * kFragBytes * t);
+    for (int j = 0; j < kDmaPerWave; ++j) {
+      const uint32_t band = static_cast<uint32_t>(min(m0 / 32 + rband[j], mbands - 1));
+      dma16(rsx, dst + 64 * j, band * band_bytes + rpart[j], 2 * kFragBytes * st);
+    }
   };
-  auto load_w = [&](WFrag& w, int t) {
+  auto load_w = [&](WFrag& w, int n0, int st) __attribute__((always_inline)) {
 #pragma unroll
-    for (int s = 0; s < 2; ++s)
+    for (int f = 0; f < 2; ++f) {
+      const uint32_t wb = static_cast<uint32_t>(min(n0 / 32 + 2 * wn + f, nbands - 1)) * band_bytes;
 #pragma unroll
-      for (int f = 0; f < 2; ++f) {
-        const int so = (2 * t + s) * kFragBytes;
-        const v4i32 a = __builtin_bit_cast(v4i32, __builtin_amdgcn_raw_buffer_load_b128(rsw, wb[f] + 16 * lane, so, 0));
-        const v2i32 b = __builtin_bit_cast(v2i32, __builtin_amdgcn_raw_buffer_load_b64(rsw, wb[f] + 1024 + 8 * lane, so, 0));
+      for (int s = 0; s < 2; ++s) {
+        const int so = (2 * st + s) * kFragBytes;
+        const v4i32 a = __builtin_bit_cast(v4i32, __builtin_amdgcn_raw_buffer_load_b128(rsw, wb + 16 * lane, so, 0));
+        const v2i32 b = __builtin_bit_cast(v2i32, __builtin_amdgcn_raw_buffer_load_b64(rsw, wb + 1024 + 8 * lane, so, 0));
         w.f[s][f] = join(a, b);
       }
+    }
+  };
+  // Scales and bias of the tile at (m0, n0) into LDS: waves 0..3 take a
+  // quarter of s_x each, waves 4..7 a quarter of s_w, waves 0..1 half of the
+  // bias.  Entries past M or N read as zero (outside the buffers).
+  auto issue_scales = [&](int m0, int n0) __attribute__((always_inline)) {
+    if constexpr (EPI == Epilogue::kBf16) {
+      const int q = wave & 3;
+      if (wave < 4) {
+        const __amdgpu_buffer_rsrc_t r =
+            __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(sx), 0, 4 * M, kBufferFlags);
+        dma4(r, sc_x + 64 * q, 4 * static_cast<uint32_t>(m0 + 64 * q + lane), 0);
+      } else {
+        const __amdgpu_buffer_rsrc_t r =
+            __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(sw), 0, 4 * N, kBufferFlags);
+        dma4(r, sc_w + 64 * q, 4 * static_cast<uint32_t>(n0 + 64 * q + lane), 0);
+      }
+      if (HAS_BIAS && wave < 2) {
+        const __amdgpu_buffer_rsrc_t r =
+            __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(bias), 0, 2 * N, kBufferFlags);
+        dma4(r, reinterpret_cast<float*>(sc_b + 64 * wave), 2 * static_cast<uint32_t>(n0 + 128 * wave + 2 * lane), 0);
+      }
+    }
   };
   // B fragment (k-step s, band 4 wm + fm) from slot k: the 16-byte part and
-  // the 8-byte part, the latter read as 16 bytes whose upper half is unused.
-  auto read_b = [&](int k, int s, int fm) {
+  // the 8-byte part.
+  auto read_b = [&](int k, int s, int fm) __attribute__((always_inline)) {
     const uint8_t* p = reinterpret_cast<const uint8_t*>(slot(k)) + (s * 8 + 4 * wm + fm) * kFragBytes;
     return join(*reinterpret_cast<const v4i32*>(p + 16 * lane),
-                *reinterpret_cast<const v4i32_a8*>(p + 1024 + 8 * lane));
+                *reinterpret_cast<const v2i32*>(p + 1024 + 8 * lane));
   };
 
   v16f acc[2][4];
@@ -344,16 +387,37 @@ __global__ __launch_bounds__(kF6Threads, 1) void w4a4_f6_gemm_kernel(
 #pragma unroll
     for (int fm = 0; fm < 4; ++fm) acc[f][fm] = v16f{};
 
-  // Prologue: weights of stage 0, activations of stages 0..2.  Loads for
-  // stages past the last one are issued anyway, for the last stage again
-  // (every address stays inside the operands): the weights land in a register
-  // set that is not used again and the activations in a slot whose data is
-  // not read, which keeps the wait counts below constant.
+  // The block walks one stream of stages g = i * T + t over its tiles i.
+  // Loads run ahead across tile boundaries: the weights of stage g + 1 and
+  // the activations of stage g + 3.  Past the block's last stage they are
+  // issued anyway, for its last stage again (every address stays inside the
+  // operands), which keeps the wait counts below constant.
+  int cm0, cn0, xm0, xn0;  // current and next tile
+  tile_at(0, &cm0, &cn0);
+  if (ntiles > 1) tile_at(1, &xm0, &xn0);
+  else xm0 = cm0, xn0 = cn0;
+  // Tile and stage of g + k for k < 2T, clamped to the block's last stage.
+  auto ahead = [&](int t, int ti, int k, int* m0, int* n0, int* st) __attribute__((always_inline)) {
+    const int u = t + k;
+    if (u < T) {
+      *m0 = cm0, *n0 = cn0, *st = u;
+    } else if (ti + 1 < ntiles) {
+      *m0 = xm0, *n0 = xn0, *st = min(u - T, last);
+    } else {
+      *m0 = cm0, *n0 = cn0, *st = last;
+    }
+  };
+
   WFrag w0, w1;
-  load_w(w0, 0);
-  issue_dma(0, 0);
-  issue_dma(min(1, last), 1);
-  issue_dma(min(2, last), 2);
+  {
+    int m0, n0, st;
+    load_w(w0, cn0, 0);
+    issue_dma(cm0, 0, 0);
+    ahead(0, 0, 1, &m0, &n0, &st);
+    issue_dma(m0, st, 1);
+    ahead(0, 0, 2, &m0, &n0, &st);
+    issue_dma(m0, st, 2);
+  }
   __builtin_amdgcn_s_waitcnt(vmcnt_imm(2 * kDmaPerWave));  // DMA(0)
   __builtin_amdgcn_s_barrier();
   __builtin_amdgcn_sched_barrier(0);
@@ -362,19 +426,136 @@ __global__ __launch_bounds__(kF6Threads, 1) void w4a4_f6_gemm_kernel(
   // MFMAs of fragment i - 4 run.
   v8i bq0 = read_b(0, 0, 0), bq1 = read_b(0, 0, 1), bq2 = read_b(0, 0, 2), bq3 = read_b(0, 0, 3);
 
-  // One stage t = t0 + I, t0 a multiple of 6: slot I % 3 and weight set
-  // I % 2, both known at compile time.  The stage starts by loading stage
-  // t + 1's weights into the other set (done with at stage t - 1).  Half way
-  // through, once every wave has read the whole slot (lgkmcnt(0) + barrier)
-  // and DMA(t + 1) has landed, the slot takes the DMA of stage t + 3.  The
-  // wait there, vmcnt(11), leaves in flight exactly the loads issued since
-  // stage t's weights: DMA(t + 2) and stage t + 1's weights.
+  // Epilogue of the current tile: lane holds column m = m0 + 128 wm + 32 fm +
+  // (lane & 31) and rows n = n0 + 64 wn + 32 f + 8 j + 4 (lane >> 5) + r of
+  // y^T.  Then the accumulators restart from zero.
+  auto epilogue = [&]() __attribute__((always_inline)) {
+    const int mb = cm0 + 128 * wm + (lane & 31);
+    const int nl = 64 * wn + 4 * (lane >> 5);  // within the tile
+    const bool full = (cm0 + kFBM <= M) && (cn0 + kFBN <= N) && (N % 4 == 0);
+    if constexpr (EPI == Epilogue::kInt32) {
+      int32_t* o = static_cast<int32_t*>(out);
+#pragma unroll
+      for (int f = 0; f < 2; ++f)
+#pragma unroll
+        for (int fm = 0; fm < 4; ++fm) {
+          const int m = mb + 32 * fm;
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const int n = cn0 + nl + 32 * f + 8 * j;
+            const int v0 = static_cast<int>(acc[f][fm][4 * j]), v1 = static_cast<int>(acc[f][fm][4 * j + 1]);
+            const int v2 = static_cast<int>(acc[f][fm][4 * j + 2]), v3 = static_cast<int>(acc[f][fm][4 * j + 3]);
+            int32_t* p = o + static_cast<int64_t>(m) * N + n;
+            if (full) {
+              *reinterpret_cast<int4*>(p) = make_int4(v0, v1, v2, v3);
+            } else if (m < M) {
+              if (n + 0 < N) p[0] = v0;
+              if (n + 1 < N) p[1] = v1;
+              if (n + 2 < N) p[2] = v2;
+              if (n + 3 < N) p[3] = v3;
+            }
+          }
+        }
+    } else {
+      // Through LDS: a wave's 128 x 64 outputs in two halves of 64 rows; each
+      // half is written to LDS as the accumulators hold it and stored to
+      // memory as whole 128-byte rows, eight rows per instruction (in a ragged
+      // tile, element by element where a row runs past M or N).
+      uint16_t* o = static_cast<uint16_t*>(out);
+      uint8_t* sb = reinterpret_cast<uint8_t*>(stg[wave]);
+      const bool vec = full && (N % 8 == 0);
+#pragma unroll
+      for (int ph = 0; ph < 2; ++ph) {
+#pragma unroll
+        for (int f = 0; f < 2; ++f)
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const int c = nl + 32 * f + 8 * j;  // column within the tile
+            const float4 swv = *reinterpret_cast<const float4*>(sc_w + c);
+            const float swa[4] = {swv.x, swv.y, swv.z, swv.w};
+            float bv[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+            if (HAS_BIAS) {
+              if (full) {
+                const uint2 bb = *reinterpret_cast<const uint2*>(sc_b + c / 2);
+                bv[0] = __uint_as_float(bb.x << 16);
+                bv[1] = __uint_as_float(bb.x & 0xFFFF0000u);
+                bv[2] = __uint_as_float(bb.y << 16);
+                bv[3] = __uint_as_float(bb.y & 0xFFFF0000u);
+              } else {
+                // a ragged tile (with odd N the last staged pair of bias values
+                // reads past the buffer as zero): straight from memory
+#pragma unroll
+                for (int r = 0; r < 4; ++r)
+                  bv[r] = __uint_as_float(static_cast<uint32_t>(bias[min(cn0 + c + r, N - 1)]) << 16);
+              }
+            }
+#pragma unroll
+            for (int fh = 0; fh < 2; ++fh) {
+              const int fm = 2 * ph + fh;
+              const float sxv = sc_x[128 * wm + 32 * fm + (lane & 31)];
+              uint16_t h[4];
+#pragma unroll
+              for (int r = 0; r < 4; ++r) {
+                float v = acc[f][fm][4 * j + r];
+                v = v * sxv;
+                v = v * swa[r];
+                if (HAS_BIAS) v = v + bv[r];
+                h[r] = __builtin_bit_cast(uint16_t, static_cast<__bf16>(v));
+              }
+              const int row = 32 * fh + (lane & 31);
+              const int col = c - 64 * wn;  // within the wave's 64 columns
+              const int chunk = (col >> 3) ^ ((row >> 1) & 7);
+              *reinterpret_cast<uint2*>(sb + 128 * row + 16 * chunk + 2 * (col & 7)) =
+                  make_uint2(h[0] | (static_cast<uint32_t>(h[1]) << 16), h[2] | (static_cast<uint32_t>(h[3]) << 16));
+            }
+          }
+        __builtin_amdgcn_wave_barrier();
+#pragma unroll
+        for (int it = 0; it < 8; ++it) {
+          const int row = 8 * it + (lane >> 3);
+          const int c = lane & 7;
+          const uint4 v = *reinterpret_cast<const uint4*>(sb + 128 * row + 16 * (c ^ ((row >> 1) & 7)));
+          const int m = cm0 + 128 * wm + 64 * ph + row;
+          const int n = cn0 + 64 * wn + 8 * c;
+          uint16_t* p = o + static_cast<int64_t>(m) * N + n;
+          if (vec) {
+            *reinterpret_cast<uint4*>(p) = v;
+          } else if (m < M) {
+            const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+              if (n + e < N) p[e] = static_cast<uint16_t>(w[e >> 1] >> (16 * (e & 1)));
+          }
+        }
+        __builtin_amdgcn_wave_barrier();
+      }
+    }
+#pragma unroll
+    for (int f = 0; f < 2; ++f)
+#pragma unroll
+      for (int fm = 0; fm < 4; ++fm) acc[f][fm] = v16f{};
+  };
+
+  // One stage g = g0 + I, g0 a multiple of 6: slot I % 3 and weight set
+  // I % 2, both known at compile time; t is its stage within tile ti.  The
+  // stage starts by loading stage g + 1's weights into the other set (done
+  // with at stage g - 1).  Half way through, once every wave has read the
+  // whole slot (lgkmcnt(0) + barrier) and DMA(g + 1) has landed, the slot
+  // takes the DMA of stage g + 3 (at a tile's first stage, the tile's scales
+  // are moved first).  The wait there, vmcnt(11), leaves in flight exactly
+  // the loads issued since stage g's weights: DMA(g + 2) and stage g + 1's
+  // weights.  After a tile's last stage comes its epilogue.
   WFrag* wset[2] = {&w0, &w1};
-  auto stage = [&](int t, auto I) {
+  int t = 0, ti = 0;
+  auto stage = [&](auto I) __attribute__((always_inline)) {
     constexpr int i = decltype(I)::value;
     constexpr int cur = i % 3, nxt = (i + 1) % 3;
     const WFrag& wc = *wset[i % 2];
-    load_w(*wset[(i + 1) % 2], min(t + 1, last));
+    {
+      int m0, n0, st;
+      ahead(t, ti, 1, &m0, &n0, &st);
+      load_w(*wset[(i + 1) % 2], n0, st);
+    }
 #define JQ_F6_STEP(S, FM, BQ, NK, NS, NFM)                                                            \
   acc[0][FM] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(wc.f[S][0], BQ, acc[0][FM], 3, 3, 0, 127, \
                                                                 0, 127);                              \
@@ -391,95 +572,45 @@ __global__ __launch_bounds__(kF6Threads, 1) void w4a4_f6_gemm_kernel(
     __builtin_amdgcn_s_waitcnt(vmcnt_imm(kWLoads + kDmaPerWave));
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
-    issue_dma(min(t + 3, last), cur);
+    if (t == 0) issue_scales(cm0, cn0);
+    {
+      int m0, n0, st;
+      ahead(t, ti, 3, &m0, &n0, &st);
+      issue_dma(m0, st, cur);
+    }
     // k-step 1; the window moves on to k-step 0 of the next stage (past the
-    // last stage these reads are of a slot whose data is not used)
+    // block's last stage these reads are of a slot whose data is not used)
     JQ_F6_STEP(1, 0, bq0, nxt, 0, 0)
     JQ_F6_STEP(1, 1, bq1, nxt, 0, 1)
     JQ_F6_STEP(1, 2, bq2, nxt, 0, 2)
     JQ_F6_STEP(1, 3, bq3, nxt, 0, 3)
 #undef JQ_F6_STEP
     __builtin_amdgcn_sched_barrier(0);
+    if (t == last) {
+      if (T == 1) {
+        // the scales were moved at this very stage
+        __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+        __builtin_amdgcn_s_barrier();
+      }
+      epilogue();
+      ++ti;
+      t = 0;
+      cm0 = xm0, cn0 = xn0;
+      if (ti + 1 < ntiles) tile_at(ti + 1, &xm0, &xn0);
+    } else {
+      ++t;
+    }
   };
-  for (int t = 0; t < T; t += 6) {
-    stage(t, std::integral_constant<int, 0>{});
+  const int G = ntiles * T;
+  for (int g = 0; g < G; g += 6) {
+    stage(std::integral_constant<int, 0>{});
 #define JQ_F6_NEXT(N) \
-    if (t + N < T) stage(t + N, std::integral_constant<int, N>{});
+    if (g + N < G) stage(std::integral_constant<int, N>{});
     JQ_F6_NEXT(1) JQ_F6_NEXT(2) JQ_F6_NEXT(3) JQ_F6_NEXT(4) JQ_F6_NEXT(5)
 #undef JQ_F6_NEXT
   }
   // no load may still be writing LDS or registers when the wave ends
   __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
-
-  // Epilogue: lane holds column m = m0 + 128 wm + 32 fm + (lane & 31) and
-  // rows n = n0 + 64 wn + 32 f + 8 j + 4 (lane >> 5) + r of y^T.
-  const int mb = m0 + 128 * wm + (lane & 31);
-  const int nb = n0 + 64 * wn + 4 * (lane >> 5);
-  const bool full = (m0 + kFBM <= M) && (n0 + kFBN <= N) && (N % 4 == 0);
-  if constexpr (EPI == Epilogue::kInt32) {
-    int32_t* o = static_cast<int32_t*>(out);
-#pragma unroll
-    for (int f = 0; f < 2; ++f)
-#pragma unroll
-      for (int fm = 0; fm < 4; ++fm) {
-        const int m = mb + 32 * fm;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int n = nb + 32 * f + 8 * j;
-          const int v0 = static_cast<int>(acc[f][fm][4 * j]), v1 = static_cast<int>(acc[f][fm][4 * j + 1]);
-          const int v2 = static_cast<int>(acc[f][fm][4 * j + 2]), v3 = static_cast<int>(acc[f][fm][4 * j + 3]);
-          int32_t* p = o + static_cast<int64_t>(m) * N + n;
-          if (full) {
-            *reinterpret_cast<int4*>(p) = make_int4(v0, v1, v2, v3);
-          } else if (m < M) {
-            if (n + 0 < N) p[0] = v0;
-            if (n + 1 < N) p[1] = v1;
-            if (n + 2 < N) p[2] = v2;
-            if (n + 3 < N) p[3] = v3;
-          }
-        }
-      }
-  } else {
-    uint16_t* o = static_cast<uint16_t*>(out);
-    float sxv[4];
-#pragma unroll
-    for (int fm = 0; fm < 4; ++fm) sxv[fm] = sx[min(mb + 32 * fm, M - 1)];
-#pragma unroll
-    for (int f = 0; f < 2; ++f)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int n = nb + 32 * f + 8 * j;
-        float swv[4], bv[4];
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int nn = min(n + r, N - 1);
-          swv[r] = sw[nn];
-          bv[r] = HAS_BIAS ? __uint_as_float(static_cast<uint32_t>(bias[nn]) << 16) : 0.0f;
-        }
-#pragma unroll
-        for (int fm = 0; fm < 4; ++fm) {
-          const int m = mb + 32 * fm;
-          uint16_t h[4];
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            float v = acc[f][fm][4 * j + r];
-            v = v * sxv[fm];
-            v = v * swv[r];
-            if (HAS_BIAS) v = v + bv[r];
-            h[r] = __builtin_bit_cast(uint16_t, static_cast<__bf16>(v));
-          }
-          uint16_t* p = o + static_cast<int64_t>(m) * N + n;
-          if (full) {
-            *reinterpret_cast<uint2*>(p) = make_uint2(h[0] | (static_cast<uint32_t>(h[1]) << 16),
-                                                      h[2] | (static_cast<uint32_t>(h[3]) << 16));
-          } else if (m < M) {
-#pragma unroll
-            for (int r = 0; r < 4; ++r)
-              if (n + r < N) p[r] = h[r];
-          }
-        }
-      }
-  }
 }
 
 template <int NJ>
@@ -527,14 +658,22 @@ hipError_t launch_w4a4_f6_gemm(Epilogue epi, const uint8_t* xf6, const float* sx
   const int tiles_n = static_cast<int>((N + kFBN - 1) / kFBN);
   const int64_t T = static_cast<int64_t>(tiles_m) * tiles_n;
   const int64_t per_xcd = (T + kNumXcd - 1) / kNumXcd;
-  const dim3 grid(static_cast<unsigned>(per_xcd * kNumXcd));
+  // One block per CU at most (a block fills a CU's registers); each walks
+  // its tiles in turn.
+  int dev = 0, cus = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+  if (e != hipSuccess) return e;
   const int ksteps = static_cast<int>(f6_ksteps(K));
+  const int64_t slots = std::max<int64_t>(kNumXcd, cus / kNumXcd * kNumXcd);
+  const int blocks = static_cast<int>(ksteps / 2 < 3 ? per_xcd * kNumXcd : std::min<int64_t>(per_xcd * kNumXcd, slots));
   const int mbands = static_cast<int>((M + 31) / 32);
   const int nbands = static_cast<int>((N + 31) / 32);
   const int Mi = static_cast<int>(M), Ni = static_cast<int>(N);
-#define JQ_F6(E, B)                                                                                              \
-  hipLaunchKernelGGL((w4a4_f6_gemm_kernel<E, B>), grid, dim3(kF6Threads), 0, st, xf6, sx, Mi, mbands, wf6, sw, Ni, \
-                     nbands, ksteps, bias, out, tiles_m, tiles_n)
+#define JQ_F6(E, B)                                                                                     \
+  hipLaunchKernelGGL((w4a4_f6_gemm_kernel<E, B>), dim3(blocks), dim3(kF6Threads), 0, st, xf6, sx, Mi, mbands, \
+                     wf6, sw, Ni, nbands, ksteps, bias, out, tiles_m, tiles_n, blocks)
   if (epi == Epilogue::kInt32) JQ_F6(Epilogue::kInt32, false);
   else if (bias != nullptr) JQ_F6(Epilogue::kBf16, true);
   else JQ_F6(Epilogue::kBf16, false);

@@ -193,6 +193,20 @@ def test_f6_gemm_i32_random_codes(M, N, K):
     assert bad.size == 0, f"{len(bad)} accumulators differ, first {bad[:4].tolist()}"
 
 
+@pytest.mark.parametrize("M,N,K", [(4096, 8192, 384), (2100, 9000, 448), (4608, 4096, 256), (300, 70000, 512)])
+def test_f6_gemm_i32_several_tiles_per_block(M, N, K):
+    """More tiles than CUs: blocks walk several tiles, with loads running
+    ahead across tile boundaries (three or more stages per tile), or one tile
+    each (fewer than three stages)."""
+    say("f6 gemm i32 many tiles", M, N, K)
+    qx = rand_packed(M, K, seed=M + 2 * K)
+    qw = rand_packed(N, K, seed=N + 3 * K)
+    got = f6_i32(qx, qw)
+    ref = oracle.w4a4_gemm_i32(qx, qw)
+    bad = np.argwhere(got != ref)
+    assert bad.size == 0, f"{len(bad)} accumulators differ, first {bad[:4].tolist()}"
+
+
 @pytest.mark.parametrize("code_x,code_w", [(-8, -8), (7, -8), (-7, 7)])
 def test_f6_gemm_i32_extreme_codes_max_k(code_x, code_w):
     K, M, N = 65536, 300, 260
