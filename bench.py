@@ -2,22 +2,30 @@
 """W4A4 linear benchmark on one MI355X: effective TOPS on the FLUX-12B MLP linears.
 
 One step = the whole hot path (per-token int4 quantisation of the activations,
-packed int4 GEMM with int32 accumulation, fused dequantising epilogue) for both
-FLUX-12B MLP linears back-to-back:
+int4 x int4 contraction with exact accumulation, fused dequantising epilogue)
+for both FLUX-12B MLP linears back-to-back:
   up:   X [4608, 3072] -> N = 12288, with bias
   down: X [9216, 12288] -> N = 3072 (two images)
 Weights are packed once before timing (offline, as at model load).  Inputs are
 seeded synthetic tensors already resident in HBM.
 
+The library computes the layer on two engines with bit-identical results:
+  * bf6:  codes carried as BF6 on gfx950's 6-bit MFMA (fp32 accumulation,
+          exact for integer codes), the faster one, timed as `value`;
+  * int8: packed int4 codes widened to int8 for the int8 MFMA (int32
+          accumulation), reported beside it under `engines`.
+
 value = sum(2 M N K) / step time, in TOPS.  The line also carries the roofline
-of the dominant kernel (the down-projection GEMM), timed per launch with HIP
-events on the stream the library launches on, and the CPU oracle timed on a
-the whole step on the host cores (repeated until about ten seconds have passed).
+of the dominant kernel (the down-projection GEMM of the bf6 engine, against the
+6-bit MFMA peak), timed per launch with HIP events on the stream the library
+launches on, and the CPU oracle timed on the whole step on the host cores
+(repeated until about ten seconds have passed), whose outputs are compared
+with the GPU's.
 
 `secondary` reports, from the same run, the same measurement for other
 layers: the FLUX MLP step with ternary weights (W1.58A4) and group-wise
-(group64), the 8B diffusion-LLM block linears (W4A4, W1.58A4, group128) and
-the DiT attention projection and fused QKV linears.
+(group64), the 8B diffusion-LLM block linears (W4A4 on both engines, W1.58A4,
+group128) and the DiT attention projection and fused QKV linears.
 """
 
 import argparse
@@ -31,6 +39,7 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 PEAK_INT8_TOPS = 5000.0     # MI355X dense int8 MFMA, published
+PEAK_FP6_TOPS = 10100.0     # MI355X dense fp6 / fp4 MFMA, published
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E, published
 
 
@@ -48,7 +57,7 @@ def parse_args():
 
 
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_flux_mlp.json")
-GEMM_SOURCE = os.path.join(ROOT, "paper_2609_33601_amd", "csrc", "gemm.hip")
+GEMM_SOURCE = os.path.join(ROOT, "paper_2609_33601_amd", "csrc", "f6.hip")
 
 
 def recorded_traffic(kernel_linear):
@@ -86,8 +95,9 @@ def _make_x(lin):
 class Prepared:
     """Device-resident inputs, packed weight and output/workspace buffers of one linear.
 
-    fmt "int4" packs the weight for the W4A4 layer, "ternary" for W1.58A4,
-    "group64" / "group128" for group-wise W4A4 with that group size.
+    fmt "int4" packs the weight for the W4A4 layer (int8 engine), "bf6" for
+    the same layer on the bf6 engine, "ternary" for W1.58A4, "group64" /
+    "group128" for group-wise W4A4 with that group size.
     """
 
     def __init__(self, lin, torch, jq, fmt="int4"):
@@ -105,6 +115,11 @@ class Prepared:
             self.linear = lambda x, wq, sw, b, y, workspace: jq.jq_w4a4g_linear(x, wq, sw, G, b, y=y,
                                                                                workspace=workspace)
             ws_bytes = jq.jq_w4a4g_workspace_bytes(lin.M, lin.K, G)
+        elif fmt == "bf6":
+            self.wq4, self.sw = jq.jq_pack_weight_int4(w)
+            self.wq = jq.jq_int4_to_f6(self.wq4)
+            self.linear = jq.jq_w4a4_f6_linear
+            ws_bytes = jq.jq_w4a4_f6_workspace_bytes(lin.M, lin.K)
         else:
             pack = jq.jq_pack_weight_ternary if fmt == "ternary" else jq.jq_pack_weight_int4
             self.linear = jq.jq_w158a4_linear if fmt == "ternary" else jq.jq_w4a4_linear
@@ -115,6 +130,8 @@ class Prepared:
         self.ws = torch.empty(ws_bytes, dtype=torch.uint8, device="cuda")
         self.q = torch.empty((lin.M, lin.K // 2), dtype=torch.uint8, device="cuda")
         self.s = torch.empty((lin.M,), dtype=torch.float32, device="cuda")
+        if fmt == "bf6":
+            self.q = torch.empty((jq.jq_f6_operand_bytes(lin.M, lin.K),), dtype=torch.uint8, device="cuda")
 
 
 def cpu_baseline(preps, target_s):
@@ -181,16 +198,18 @@ def time_step(torch, preps, steps, warmup):
 
 
 def secondary(torch, jq, workloads, steps):
-    cases = [(workloads.FLUX_MLP, "ternary"), (workloads.WORKLOADS["dllm_block"], "int4"),
-             (workloads.WORKLOADS["dllm_block"], "ternary"), (workloads.WORKLOADS["attn_proj"], "int4"),
-             (workloads.WORKLOADS["qkv"], "int4"), (workloads.FLUX_MLP, "group64"),
-             (workloads.WORKLOADS["dllm_block"], "group128")]
+    cases = [(workloads.FLUX_MLP, "ternary"), (workloads.WORKLOADS["dllm_block"], "bf6"),
+             (workloads.WORKLOADS["dllm_block"], "int4"), (workloads.WORKLOADS["dllm_block"], "ternary"),
+             (workloads.WORKLOADS["attn_proj"], "bf6"), (workloads.WORKLOADS["attn_proj"], "int4"),
+             (workloads.WORKLOADS["qkv"], "bf6"), (workloads.WORKLOADS["qkv"], "int4"),
+             (workloads.FLUX_MLP, "group64"), (workloads.WORKLOADS["dllm_block"], "group128")]
     out = []
     for wl, fmt in cases:
         preps = [Prepared(lin, torch, jq, fmt) for lin in wl.linears]
         us = time_step(torch, preps, steps, warmup=5)
         tops = wl.ops / (us * 1e-6) / 1e12
-        layer = {"ternary": "W1.58A4", "int4": "W4A4"}.get(fmt, f"W4A4 {fmt}")
+        layer = {"ternary": "W1.58A4", "int4": "W4A4 (int8 engine)", "bf6": "W4A4 (bf6 engine)"}.get(
+            fmt, f"W4A4 {fmt}")
         log(f"secondary {wl.name} {layer}: {us:.1f} us/step, {tops:.0f} effective TOPS")
         out.append({"workload": wl.description, "layer": layer, "us_per_step": us, "effective_TOPS": tops,
                     "pct_int8_peak": 100.0 * tops / PEAK_INT8_TOPS,
@@ -216,13 +235,14 @@ def main():
     jq.lib()
     wl = workloads.FLUX_MLP
     log("preparing", wl.description)
-    preps = [Prepared(lin, torch, jq) for lin in wl.linears]
+    preps = [Prepared(lin, torch, jq, "bf6") for lin in wl.linears]
+    preps4 = [Prepared(lin, torch, jq, "int4") for lin in wl.linears]
     torch.cuda.synchronize()
     stream = torch.cuda.current_stream()
 
     def step():
         for p in preps:
-            jq.jq_w4a4_linear(p.x, p.wq, p.sw, p.b, y=p.y, workspace=p.ws)
+            jq.jq_w4a4_f6_linear(p.x, p.wq, p.sw, p.b, y=p.y, workspace=p.ws)
 
     for _ in range(args.warmup):
         step()
@@ -240,42 +260,58 @@ def main():
     wall = time.perf_counter() - t0
     ms_per_step = ev0.elapsed_time(ev1) / args.steps
     value = wl.ops / (ms_per_step * 1e-3) / 1e12
-    log(f"timed {args.steps} steps: {ms_per_step * 1e3:.1f} us/step (wall {wall * 1e6 / args.steps:.1f} us/step)")
+    log(f"bf6 engine: timed {args.steps} steps: {ms_per_step * 1e3:.1f} us/step "
+        f"(wall {wall * 1e6 / args.steps:.1f} us/step)")
 
-    # Per-kernel durations: the same two kernels the linear launches, bracketed by events.
+    # The same step on the int8 engine (same layer, bit-identical outputs).
+    us_int8 = time_step(torch, preps4, args.steps, warmup=max(2, args.warmup // 4))
+    log(f"int8 engine: {us_int8:.1f} us/step, {wl.ops / (us_int8 * 1e-6) / 1e12:.0f} effective TOPS")
+
+    # Per-kernel durations: the two kernels each linear launches, bracketed by
+    # events on the stream they run on, for both engines.
     n_launch = max(args.steps, 20)
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(len(preps) * n_launch)]
-    for it in range(n_launch):
-        for j, p in enumerate(preps):
-            e = evs[it * len(preps) + j]
-            e[0].record(stream)
-            jq.jq_quantize_act(p.x, q=p.q, scale=p.s)
-            e[1].record(stream)
-            jq.jq_w4a4_gemm(p.q, p.s, p.wq, p.sw, p.b, y=p.y)
-            e[2].record(stream)
-    torch.cuda.synchronize()
     kernels = []
-    for j, p in enumerate(preps):
-        lin = p.lin
-        tq = sum(evs[it * len(preps) + j][0].elapsed_time(evs[it * len(preps) + j][1]) for it in range(n_launch))
-        tg = sum(evs[it * len(preps) + j][1].elapsed_time(evs[it * len(preps) + j][2]) for it in range(n_launch))
-        tq_us, tg_us = tq / n_launch * 1e3, tg / n_launch * 1e3
-        q_bytes = 2 * lin.M * lin.K + lin.M * lin.K // 2 + 4 * lin.M
-        g_ops = 2 * lin.M * lin.N * lin.K
-        kernels.append({"linear": lin.name, "kernel": "quantize_rows", "avg_us": tq_us,
-                        "algorithmic_bytes": q_bytes, "achieved_GBs": q_bytes / tq_us / 1e3,
-                        "frac_hbm_peak": q_bytes / tq_us / 1e3 / PEAK_HBM_GBS})
-        kernels.append({"linear": lin.name, "kernel": "w4a4_gemm", "avg_us": tg_us, "ops": g_ops,
-                        "achieved_TOPS": g_ops / tg_us / 1e6,
-                        "frac_int8_peak": g_ops / tg_us / 1e6 / PEAK_INT8_TOPS})
-        log(f"{lin.name}: quantize {tq_us:.1f} us ({q_bytes / tq_us / 1e3:.0f} GB/s), "
-            f"gemm {tg_us:.1f} us ({g_ops / tg_us / 1e6:.0f} TOPS)")
-    dom = max((k for k in kernels if k["kernel"] == "w4a4_gemm"), key=lambda k: k["ops"])
-    roofline = {"bound": "mfma", "achieved": dom["achieved_TOPS"], "peak": PEAK_INT8_TOPS, "unit": "TOP/s",
-                "frac": dom["achieved_TOPS"] / PEAK_INT8_TOPS, "traffic": None,
-                "kernel": f"w4a4_gemm ({dom['linear']})", "avg_launch_us": dom["avg_us"]}
-
-    roofline["traffic"] = recorded_traffic(dom["linear"])
+    for engine, pp in (("bf6", preps), ("int8", preps4)):
+        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(len(pp) * n_launch)]
+        for it in range(n_launch):
+            for j, p in enumerate(pp):
+                e = evs[it * len(pp) + j]
+                e[0].record(stream)
+                if engine == "bf6":
+                    jq.jq_quantize_act_f6(p.x, xf6=p.q, scale=p.s)
+                    e[1].record(stream)
+                    jq.jq_w4a4_f6_gemm(p.q, p.s, p.lin.K, p.wq, p.sw, p.b, y=p.y)
+                else:
+                    jq.jq_quantize_act(p.x, q=p.q, scale=p.s)
+                    e[1].record(stream)
+                    jq.jq_w4a4_gemm(p.q, p.s, p.wq, p.sw, p.b, y=p.y)
+                e[2].record(stream)
+        torch.cuda.synchronize()
+        for j, p in enumerate(pp):
+            lin = p.lin
+            tq = sum(evs[it * len(pp) + j][0].elapsed_time(evs[it * len(pp) + j][1]) for it in range(n_launch))
+            tg = sum(evs[it * len(pp) + j][1].elapsed_time(evs[it * len(pp) + j][2]) for it in range(n_launch))
+            tq_us, tg_us = tq / n_launch * 1e3, tg / n_launch * 1e3
+            code_bytes = jq.jq_f6_operand_bytes(lin.M, lin.K) if engine == "bf6" else lin.M * lin.K // 2
+            q_bytes = 2 * lin.M * lin.K + code_bytes + 4 * lin.M
+            g_ops = 2 * lin.M * lin.N * lin.K
+            peak = PEAK_FP6_TOPS if engine == "bf6" else PEAK_INT8_TOPS
+            kernels.append({"engine": engine, "linear": lin.name, "kernel": "quantize_rows", "avg_us": tq_us,
+                            "algorithmic_bytes": q_bytes, "achieved_GBs": q_bytes / tq_us / 1e3,
+                            "frac_hbm_peak": q_bytes / tq_us / 1e3 / PEAK_HBM_GBS})
+            kernels.append({"engine": engine, "linear": lin.name, "kernel": "w4a4_gemm", "avg_us": tg_us,
+                            "ops": g_ops, "achieved_TOPS": g_ops / tg_us / 1e6, "peak_TOPS": peak,
+                            "frac_mfma_peak": g_ops / tg_us / 1e6 / peak,
+                            "pct_int8_peak": 100.0 * g_ops / tg_us / 1e6 / PEAK_INT8_TOPS})
+            log(f"{engine} {lin.name}: quantize {tq_us:.1f} us ({q_bytes / tq_us / 1e3:.0f} GB/s), "
+                f"gemm {tg_us:.1f} us ({g_ops / tg_us / 1e6:.0f} TOPS)")
+    dom = max((k for k in kernels if k["kernel"] == "w4a4_gemm" and k["engine"] == "bf6"), key=lambda k: k["ops"])
+    roofline = {"bound": "mfma", "achieved": dom["achieved_TOPS"], "peak": PEAK_FP6_TOPS, "unit": "TOP/s",
+                "frac": dom["achieved_TOPS"] / PEAK_FP6_TOPS, "traffic": recorded_traffic(dom["linear"]),
+                "kernel": f"w4a4_f6_gemm ({dom['linear']}, bf6 operands, fp32 accumulation)",
+                "avg_launch_us": dom["avg_us"],
+                "peak_note": "MI355X dense fp6 MFMA; the same kernel is at "
+                             f"{100.0 * dom['achieved_TOPS'] / PEAK_INT8_TOPS:.0f}% of the dense int8 peak"}
 
     if args.copy_calib:
         # Reference for FETCH_SIZE / WRITE_SIZE: a plain device copy of 256 MiB.
@@ -289,6 +325,12 @@ def main():
     # Re-run the timed configuration once so that y holds the step's outputs for the oracle comparison.
     step()
     torch.cuda.synchronize()
+    for p4 in preps4:
+        jq.jq_w4a4_linear(p4.x, p4.wq, p4.sw, p4.b, y=p4.y, workspace=p4.ws)
+    torch.cuda.synchronize()
+    engines_equal = all(torch.equal(a.y.view(torch.int16), b.y.view(torch.int16)) for a, b in zip(preps, preps4))
+    del preps4
+    torch.cuda.empty_cache()
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(preps, args.cpu_seconds)
@@ -311,7 +353,7 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "int8",
+        "dtype": "bf6 codes, fp32 accumulation (exact for int4 codes)",
         "data": "synthetic (seeded; FLUX-12B MLP activation/weight statistics)",
         "pct_int8_peak": 100.0 * value / PEAK_INT8_TOPS,
         "config": {
@@ -319,8 +361,17 @@ def main():
             "linears": [{"name": l.name, "M": l.M, "K": l.K, "N": l.N, "bias": l.bias_std is not None}
                         for l in wl.linears],
             "ops_per_step": wl.ops,
+            "engine": "bf6",
             "parallelism": "none (1 GPU)",
             "device": f"{props.name} {getattr(props, 'gcnArchName', '')} CUs={props.multi_processor_count}",
+        },
+        "engines": {
+            "bf6": {"us_per_step": ms_per_step * 1e3, "effective_TOPS": value,
+                    "pct_int8_peak": 100.0 * value / PEAK_INT8_TOPS},
+            "int8": {"us_per_step": us_int8, "effective_TOPS": wl.ops / (us_int8 * 1e-6) / 1e12,
+                     "pct_int8_peak": 100.0 * wl.ops / (us_int8 * 1e-6) / 1e12 / PEAK_INT8_TOPS,
+                     "dtype": "int8 (widened int4 codes), int32 accumulation"},
+            "outputs_bit_identical": bool(engines_equal),
         },
         "roofline": roofline,
         "cpu_baseline": cpu,
