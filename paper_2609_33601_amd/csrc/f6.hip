@@ -257,12 +257,14 @@ constexpr int kWaitcntBase = (0x7 << 4) | (0xF << 8);  // expcnt, lgkmcnt: no wa
 constexpr int vmcnt_imm(int n) { return kWaitcntBase | (n & 0xF) | ((n >> 4) << 14); }
 constexpr int kLgkm0 = 0xC07F;                          // lgkmcnt(0), vmcnt and expcnt: no wait
 constexpr int kWLoads = 8;                              // weight loads per wave per stage
+constexpr uint32_t kOutside = 0x80000000u;              // a buffer offset past every operand
 
 template <Epilogue EPI, bool HAS_BIAS>
 __global__ __launch_bounds__(kF6Threads, 1) void w4a4_f6_gemm_kernel(
     const uint8_t* __restrict__ xf6, const float* __restrict__ sx, int M, int mbands,
     const uint8_t* __restrict__ wf6, const float* __restrict__ sw, int N, int nbands, int ksteps,
-    const uint16_t* __restrict__ bias, void* __restrict__ out, int tiles_m, int tiles_n, int grid_blocks) {
+    const uint16_t* __restrict__ bias, void* __restrict__ out, int tile_bands, int tiles_m, int tiles_n,
+    int grid_blocks) {
   // The 72 KiB ring as three separate arrays.  With the stage loop
   // unrolled by six every slot is known at compile time, so the compiler
   // can tell the slot being read from the one the DMA is writing.
@@ -281,7 +283,11 @@ __global__ __launch_bounds__(kF6Threads, 1) void w4a4_f6_gemm_kernel(
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wm = wave >> 2, wn = wave & 3;  // activation half (4 bands), weight quarter (2 bands)
+  const int wm = wave >> 2, wn = wave & 3;  // activation half, weight quarter (2 bands)
+  // A tile has tile_bands (7 or 8) bands of 32 activation rows: the first
+  // half takes four of them, the second half the rest, so each SIMD (one wave
+  // of each half) does the same work whatever the tile height.
+  const int tile_rows = 32 * tile_bands;
   const int T = ksteps / 2;                  // stages of 128 codes per tile
   const int last = T - 1;
 
@@ -301,7 +307,7 @@ __global__ __launch_bounds__(kF6Threads, 1) void w4a4_f6_gemm_kernel(
   auto tile_at = [&](int i, int* m0, int* n0) __attribute__((always_inline)) {
     TileCoord tc;
     tile_of_block(blockIdx.x + i * grid_blocks, tiles_m, tiles_n, &tc);
-    *m0 = tc.tm * kFBM;
+    *m0 = tc.tm * tile_rows;
     *n0 = tc.tn * kFBN;
   };
 
@@ -317,7 +323,8 @@ __global__ __launch_bounds__(kF6Threads, 1) void w4a4_f6_gemm_kernel(
   // Q = 64 (3 wave + j) + lane of the stage is byte 16 (Q % 96) of fragment
   // Q / 96.  Per lane: the band within the tile and the byte offset within
   // the band's stage.  Bands past the operand are clamped (their results are
-  // discarded).
+  // discarded); bands past the tile get an offset outside the operand, which
+  // the buffer load answers with zeros without touching memory.
   int rband[kDmaPerWave];
   uint32_t rpart[kDmaPerWave];
 #pragma unroll
@@ -325,7 +332,7 @@ __global__ __launch_bounds__(kF6Threads, 1) void w4a4_f6_gemm_kernel(
     const int Q = 64 * (kDmaPerWave * wave + j) + lane;
     const int R = Q / 96, q = Q % 96;
     rband[j] = R & 7;
-    rpart[j] = (R >> 3) * kFragBytes + 16 * q;
+    rpart[j] = (R & 7) < tile_bands ? (R >> 3) * kFragBytes + 16 * q : kOutside;
   }
   const uint32_t band_bytes = static_cast<uint32_t>(ksteps) * kFragBytes;
 
@@ -335,7 +342,7 @@ __global__ __launch_bounds__(kF6Threads, 1) void w4a4_f6_gemm_kernel(
 #pragma unroll
     for (int j = 0; j < kDmaPerWave; ++j) {
       const uint32_t band = static_cast<uint32_t>(min(m0 / 32 + rband[j], mbands - 1));
-      dma16(rsx, dst + 64 * j, band * band_bytes + rpart[j], 2 * kFragBytes * st);
+      dma16(rsx, dst + 64 * j, rpart[j] == kOutside ? kOutside : band * band_bytes + rpart[j], 2 * kFragBytes * st);
     }
   };
   auto load_w = [&](WFrag& w, int n0, int st) __attribute__((always_inline)) {
@@ -381,6 +388,11 @@ __global__ __launch_bounds__(kF6Threads, 1) void w4a4_f6_gemm_kernel(
                 *reinterpret_cast<const v2i32*>(p + 1024 + 8 * lane));
   };
 
+  // The rest of the kernel, for a wave with NFM activation bands (four in
+  // the first half; tile_bands - 4 in the second).  Each count gets its own
+  // straight-line code, so no branch sits between the MFMAs.
+  auto run = [&](auto NFM) __attribute__((always_inline)) {
+  constexpr int nfm = decltype(NFM)::value;
   v16f acc[2][4];
 #pragma unroll
   for (int f = 0; f < 2; ++f)
@@ -430,9 +442,16 @@ __global__ __launch_bounds__(kF6Threads, 1) void w4a4_f6_gemm_kernel(
   // (lane & 31) and rows n = n0 + 64 wn + 32 f + 8 j + 4 (lane >> 5) + r of
   // y^T.  Then the accumulators restart from zero.
   auto epilogue = [&]() __attribute__((always_inline)) {
+    // The lane index is passed through an empty asm so that the per-lane
+    // addresses below are computed here, not hoisted out of the stage loop
+    // into registers the loop needs (or into scratch, whose reloads would
+    // wait for every load in flight).
+    int lane = threadIdx.x & 63;
+    asm volatile("" : "+v"(lane));
     const int mb = cm0 + 128 * wm + (lane & 31);
     const int nl = 64 * wn + 4 * (lane >> 5);  // within the tile
-    const bool full = (cm0 + kFBM <= M) && (cn0 + kFBN <= N) && (N % 4 == 0);
+    const int mlim = min(M, cm0 + tile_rows);  // rows of this tile
+    const bool full = (cm0 + tile_rows <= M) && (cn0 + kFBN <= N) && (N % 4 == 0);
     if constexpr (EPI == Epilogue::kInt32) {
       int32_t* o = static_cast<int32_t*>(out);
 #pragma unroll
@@ -440,6 +459,7 @@ __global__ __launch_bounds__(kF6Threads, 1) void w4a4_f6_gemm_kernel(
 #pragma unroll
         for (int fm = 0; fm < 4; ++fm) {
           const int m = mb + 32 * fm;
+          if (fm >= nfm) continue;
 #pragma unroll
           for (int j = 0; j < 4; ++j) {
             const int n = cn0 + nl + 32 * f + 8 * j;
@@ -448,7 +468,7 @@ __global__ __launch_bounds__(kF6Threads, 1) void w4a4_f6_gemm_kernel(
             int32_t* p = o + static_cast<int64_t>(m) * N + n;
             if (full) {
               *reinterpret_cast<int4*>(p) = make_int4(v0, v1, v2, v3);
-            } else if (m < M) {
+            } else if (m < mlim) {
               if (n + 0 < N) p[0] = v0;
               if (n + 1 < N) p[1] = v1;
               if (n + 2 < N) p[2] = v2;
@@ -466,6 +486,7 @@ __global__ __launch_bounds__(kF6Threads, 1) void w4a4_f6_gemm_kernel(
       const bool vec = full && (N % 8 == 0);
 #pragma unroll
       for (int ph = 0; ph < 2; ++ph) {
+        if (2 * ph >= nfm) break;  // a short second half (a compile-time test)
 #pragma unroll
         for (int f = 0; f < 2; ++f)
 #pragma unroll
@@ -518,9 +539,10 @@ __global__ __launch_bounds__(kF6Threads, 1) void w4a4_f6_gemm_kernel(
           const int m = cm0 + 128 * wm + 64 * ph + row;
           const int n = cn0 + 64 * wn + 8 * c;
           uint16_t* p = o + static_cast<int64_t>(m) * N + n;
-          if (vec) {
+          if (m >= mlim) {
+          } else if (vec) {
             *reinterpret_cast<uint4*>(p) = v;
-          } else if (m < M) {
+          } else {
             const uint32_t w[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
             for (int e = 0; e < 8; ++e)
@@ -556,12 +578,14 @@ __global__ __launch_bounds__(kF6Threads, 1) void w4a4_f6_gemm_kernel(
       ahead(t, ti, 1, &m0, &n0, &st);
       load_w(*wset[(i + 1) % 2], n0, st);
     }
-#define JQ_F6_STEP(S, FM, BQ, NK, NS, NFM)                                                            \
-  acc[0][FM] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(wc.f[S][0], BQ, acc[0][FM], 3, 3, 0, 127, \
-                                                                0, 127);                              \
-  acc[1][FM] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(wc.f[S][1], BQ, acc[1][FM], 3, 3, 0, 127, \
-                                                                0, 127);                              \
-  BQ = read_b(NK, NS, NFM);
+#define JQ_F6_STEP(S, FM, BQ, NK, NS, NFM)                                                              \
+  if constexpr (FM < nfm) {                                                                             \
+    acc[0][FM] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(wc.f[S][0], BQ, acc[0][FM], 3, 3, 0, 127, \
+                                                                  0, 127);                              \
+    acc[1][FM] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(wc.f[S][1], BQ, acc[1][FM], 3, 3, 0, 127, \
+                                                                  0, 127);                              \
+  }                                                                                                     \
+  if constexpr (NFM < nfm) BQ = read_b(NK, NS, NFM);
     // k-step 0; the window moves on to k-step 1 of this stage
     JQ_F6_STEP(0, 0, bq0, cur, 1, 0)
     JQ_F6_STEP(0, 1, bq1, cur, 1, 1)
@@ -611,6 +635,9 @@ __global__ __launch_bounds__(kF6Threads, 1) void w4a4_f6_gemm_kernel(
   }
   // no load may still be writing LDS or registers when the wave ends
   __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+  };
+  if (wm == 0 || tile_bands == 8) run(std::integral_constant<int, 4>{});
+  else run(std::integral_constant<int, 3>{});
 }
 
 template <int NJ>
@@ -628,6 +655,27 @@ hipError_t launch_qf6(const uint16_t* x, int64_t M, int64_t K, int64_t ksteps, u
 int64_t f6_ksteps(int64_t K) { return (K + 127) / 128 * 2; }
 
 int64_t f6_operand_bytes(int64_t rows, int64_t K) { return (rows + 31) / 32 * f6_ksteps(K) * kFragBytes; }
+
+// Tile height of the GEMM in bands of 32 rows (7 or 8).  Every tile costs its
+// height in MFMA work plus about one band's worth of fixed work (the weight
+// fragments, the epilogue); the blocks of an XCD take its tiles in rounds.
+// The height with the cheapest rounds wins, the taller one on ties: at
+// 9216 x 3072 on 256 CUs, 224-row tiles give 504 tiles in two rounds where
+// 256-row tiles give 432, which also take two rounds.
+int f6_tile_bands(int64_t M, int64_t N, int64_t slots) {
+  const int64_t tiles_n = (N + kFBN - 1) / kFBN;
+  const int64_t per_xcd_slots = std::max<int64_t>(1, slots / kNumXcd);
+  int best = 8;
+  int64_t best_cost = -1;
+  for (int b = 8; b >= 7; --b) {
+    const int64_t tiles = (M + 32 * b - 1) / (32 * b) * tiles_n;
+    const int64_t per_xcd = (tiles + kNumXcd - 1) / kNumXcd;
+    const int64_t rounds = (per_xcd + per_xcd_slots - 1) / per_xcd_slots;
+    const int64_t cost = rounds * (b + 1);
+    if (best_cost < 0 || cost < best_cost) best = b, best_cost = cost;
+  }
+  return best;
+}
 
 hipError_t launch_quantize_rows_f6(const uint16_t* x, int64_t M, int64_t K, uint8_t* out, float* scale,
                                    hipStream_t st) {
@@ -654,10 +702,6 @@ hipError_t launch_int4_to_f6(const uint8_t* q, int64_t rows, int64_t K, uint8_t*
 hipError_t launch_w4a4_f6_gemm(Epilogue epi, const uint8_t* xf6, const float* sx, int64_t M, int64_t K,
                                const uint8_t* wf6, const float* sw, int64_t N, const uint16_t* bias, void* out,
                                hipStream_t st) {
-  const int tiles_m = static_cast<int>((M + kFBM - 1) / kFBM);
-  const int tiles_n = static_cast<int>((N + kFBN - 1) / kFBN);
-  const int64_t T = static_cast<int64_t>(tiles_m) * tiles_n;
-  const int64_t per_xcd = (T + kNumXcd - 1) / kNumXcd;
   // One block per CU at most (a block fills a CU's registers); each walks
   // its tiles in turn.
   int dev = 0, cus = 0;
@@ -667,13 +711,18 @@ hipError_t launch_w4a4_f6_gemm(Epilogue epi, const uint8_t* xf6, const float* sx
   if (e != hipSuccess) return e;
   const int ksteps = static_cast<int>(f6_ksteps(K));
   const int64_t slots = std::max<int64_t>(kNumXcd, cus / kNumXcd * kNumXcd);
+  const int tile_bands = f6_tile_bands(M, N, slots);
+  const int tiles_m = static_cast<int>((M + 32 * tile_bands - 1) / (32 * tile_bands));
+  const int tiles_n = static_cast<int>((N + kFBN - 1) / kFBN);
+  const int64_t T = static_cast<int64_t>(tiles_m) * tiles_n;
+  const int64_t per_xcd = (T + kNumXcd - 1) / kNumXcd;
   const int blocks = static_cast<int>(ksteps / 2 < 3 ? per_xcd * kNumXcd : std::min<int64_t>(per_xcd * kNumXcd, slots));
   const int mbands = static_cast<int>((M + 31) / 32);
   const int nbands = static_cast<int>((N + 31) / 32);
   const int Mi = static_cast<int>(M), Ni = static_cast<int>(N);
 #define JQ_F6(E, B)                                                                                     \
   hipLaunchKernelGGL((w4a4_f6_gemm_kernel<E, B>), dim3(blocks), dim3(kF6Threads), 0, st, xf6, sx, Mi, mbands, \
-                     wf6, sw, Ni, nbands, ksteps, bias, out, tiles_m, tiles_n, blocks)
+                     wf6, sw, Ni, nbands, ksteps, bias, out, tile_bands, tiles_m, tiles_n, blocks)
   if (epi == Epilogue::kInt32) JQ_F6(Epilogue::kInt32, false);
   else if (bias != nullptr) JQ_F6(Epilogue::kBf16, true);
   else JQ_F6(Epilogue::kBf16, false);

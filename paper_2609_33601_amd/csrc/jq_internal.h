@@ -48,6 +48,8 @@ hipError_t launch_w4a4g_gemm(Epilogue epi, const uint8_t* qx, const float* sx, i
 // layout of f6_operand_bytes(rows, K) bytes (rows padded to 32, K to 128).
 int64_t f6_ksteps(int64_t K);
 int64_t f6_operand_bytes(int64_t rows, int64_t K);
+// GEMM tile height in bands of 32 rows (7 or 8) for an M x N output on `slots` CUs.
+int f6_tile_bands(int64_t M, int64_t N, int64_t slots);
 
 // Per-token quantiser writing the BF6 activation operand and the scales.
 hipError_t launch_quantize_rows_f6(const uint16_t* x, int64_t M, int64_t K, uint8_t* out, float* scale,
