@@ -117,7 +117,7 @@ class Prepared:
             ws_bytes = jq.jq_w4a4g_workspace_bytes(lin.M, lin.K, G)
         elif fmt == "bf6":
             self.wq4, self.sw = jq.jq_pack_weight_int4(w)
-            self.wq = jq.jq_int4_to_f6(self.wq4)
+            self.wq = jq.jq_int4_to_f6_weight(self.wq4)
             self.linear = jq.jq_w4a4_f6_linear
             ws_bytes = jq.jq_w4a4_f6_workspace_bytes(lin.M, lin.K)
         else:

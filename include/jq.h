@@ -314,18 +314,23 @@ jq_status jq_w4a4g_gemm_f32(const void* q_packed, const float* scales, int64_t M
  * 2^22, so the fp32 accumulators equal the exact integer ones: codes, scales,
  * accumulators and bf16 outputs are identical to the packed-int4 calls above.
  *
- * BF6 operand layout (activations and weights alike), 6 bits per code:
+ * BF6 operands, 6 bits per code:
  *   - a code c is encoded as sign bit 5 and the E3M2 magnitude
  *     |c| = (1 + m/4) * 2^(e-3) (e in bits 4..2, m in bits 1..0; 0 -> 0);
  *   - 32 codes c[0..31] form a 192-bit group, code p in bits 6p..6p+5
- *     (six little-endian dwords);
+ *     (six little-endian dwords d0..d5);
  *   - rows are padded with zero codes to a multiple of 32 and taken in bands
  *     of 32; K is padded with zero codes to a multiple of 128 and cut into
- *     KS = 2*ceil(K/128) k-steps of 64 codes;
- *   - the fragment of band b and k-step s is 1536 bytes at (b*KS + s)*1536;
- *     its bytes 24L..24L+23 (L = r + 32h, r < 32, h < 2) hold the group of
- *     codes 64s+32h .. 64s+32h+31 of row 32b + r.
- * Size: jq_f6_operand_bytes(rows, K) = ceil(rows/32) * KS * 1536.
+ *     KS = 2*ceil(K/128) k-steps of 64 codes; band b takes KS*1536 bytes at
+ *     b*KS*1536.  G(r, s, h) below is the group of codes 64s+32h ..
+ *     64s+32h+31 of row 32b + r, and L = r + 32h (r < 32, h < 2).
+ *   - Activation layout: k-step s of a band is 1536 bytes at s*1536; d0..d3
+ *     of G(r, s, h) at byte 16L, d4..d5 at byte 1024 + 8L.
+ *   - Weight layout: k-steps 2u and 2u+1 of a band share 3072 bytes at
+ *     u*3072, three planes of 1024 bytes; the 16 bytes at 1024i + 16L
+ *     (i = 0, 1, 2), in plane order, are the six dwords of G(r, 2u, h)
+ *     followed by those of G(r, 2u+1, h).
+ * Size of either: jq_f6_operand_bytes(rows, K) = ceil(rows/32) * KS * 1536.
  *
  * Shapes, alignment and errors follow the conventions at the top of this
  * file, with each BF6 operand below 2^31 bytes.
@@ -347,16 +352,24 @@ jq_status jq_quantize_act_f6(const void* x_bf16, int64_t M, int64_t K,
                              void* xf6, float* scale, void* stream);
 
 /*
- * Re-encode packed int4 codes (any codes -8..7) as a BF6 operand; lossless.
- * For weights this is done once per layer at model load, after
- * jq_pack_weight_int4, whose scales stay the weight scales.  Also serves
- * activation codes from jq_quantize_act.
+ * Re-encode packed int4 codes (any codes -8..7) as a BF6 operand in the
+ * activation layout; lossless.  Serves activation codes from
+ * jq_quantize_act (e.g. to check the GEMM on chosen codes).
  *   q_packed in   [rows,K/2] uint8, 16-byte aligned
  *   f6       out  jq_f6_operand_bytes(rows,K) bytes, 16-byte aligned
  *            (padding rows and codes are written as zeros)
  * Errors: JQ_ERR_INVALID_ARG, JQ_ERR_UNSUPPORTED_SHAPE, JQ_ERR_MISALIGNED, JQ_ERR_HIP.
  */
 jq_status jq_int4_to_f6(const void* q_packed, int64_t rows, int64_t K, void* f6, void* stream);
+
+/*
+ * The same re-encoding into the weight layout: done once per layer at model
+ * load, after jq_pack_weight_int4, whose scales stay the weight scales.
+ *   q_packed in   [rows,K/2] uint8, 16-byte aligned
+ *   wf6      out  jq_f6_operand_bytes(rows,K) bytes, 16-byte aligned
+ * Errors: as jq_int4_to_f6.
+ */
+jq_status jq_int4_to_f6_weight(const void* q_packed, int64_t rows, int64_t K, void* wf6, void* stream);
 
 /*
  * Bytes of device workspace jq_w4a4_f6_linear needs for an [M,K] input: the
@@ -370,7 +383,7 @@ size_t jq_w4a4_f6_workspace_bytes(int64_t M, int64_t K);
  * workspace (BF6 operand, then scales), then the GEMM with the fused epilogue
  * y = bf16_rne(((fl32(acc) * s_x[m]) * s_w[n]) + bias[n]).
  *   x_bf16      in   [M,K] bf16
- *   wf6         in   BF6 weight operand from jq_int4_to_f6
+ *   wf6         in   BF6 weight operand (weight layout) from jq_int4_to_f6_weight
  *   w_scale     in   [N] fp32 from jq_pack_weight_int4
  *   bias_bf16   in   [N] bf16, or NULL
  *   y_bf16      out  [M,N] bf16, 16-byte aligned
@@ -384,7 +397,8 @@ jq_status jq_w4a4_f6_linear(const void* x_bf16, int64_t M, int64_t K,
 
 /*
  * GEMM + epilogue of the BF6 engine on an already-quantised activation
- * operand (from jq_quantize_act_f6 or jq_int4_to_f6) and its scales.
+ * operand (activation layout, from jq_quantize_act_f6 or jq_int4_to_f6) and
+ * its scales; wf6 as in jq_w4a4_f6_linear.
  * Errors: JQ_ERR_INVALID_ARG, JQ_ERR_UNSUPPORTED_SHAPE, JQ_ERR_MISALIGNED, JQ_ERR_HIP.
  */
 jq_status jq_w4a4_f6_gemm(const void* xf6, const float* scale, int64_t M, int64_t K,

@@ -16,43 +16,53 @@
 //   * activations are quantised straight into BF6 by quantize_rows_f6_kernel
 //     (the same scale and codes as the packed-int4 quantiser);
 //   * weights are converted once, offline, from the canonical packed int4
-//     codes into a fragment-major BF6 layout.
+//     codes.
 //
-// BF6 operand layout (activations and weights alike).  32 codes c[0..31] form
-// a group of 192 bits, code p in bits 6p .. 6p+5 (six little-endian dwords
-// d0..d5).  Rows are padded with zero codes to a multiple of 32 and taken in
-// bands of 32; K is padded with zero codes to a multiple of 128 and cut into
-// k-steps of 64 codes (KS of them).  The fragment of band b and k-step s is
-// 1536 contiguous bytes at (b * KS + s) * 1536; lane L = r + 32h of it is the
-// group of codes 64s + 32h .. 64s + 32h + 31 of row 32b + r, with d0..d3 at
-// byte 16L and d4, d5 at byte 1024 + 8L.  That is one lane of a
-// v_mfma_*_32x32x64_f8f6f4 operand (lane L: row L % 32, one 32-code half
-// L / 32 of the instruction's 64 codes of K); A and B lanes use the same
-// assignment, so the contraction is summed correctly.  A wave loads a
-// fragment with one fully coalesced 16-byte and one 8-byte access per lane,
-// into one register tuple.
+// BF6 groups.  32 codes c[0..31] form a group of 192 bits, code p in bits
+// 6p .. 6p+5 (six little-endian dwords d0..d5).  Rows are padded with zero
+// codes to a multiple of 32 and taken in bands of 32; K is padded with zero
+// codes to a multiple of 128 and cut into k-steps of 64 codes (KS of them, an
+// even number).  Lane L = r + 32h of a v_mfma_*_32x32x64_f8f6f4 operand holds
+// the group of codes 64s + 32h .. 64s + 32h + 31 of row r of the band for
+// k-step s; A and B lanes use the same assignment, so the contraction is
+// summed correctly.  Both operands take KS * 1536 bytes per band, band b at
+// b * KS * 1536, in one of two orders within the band:
+//   * activation layout (read by the GEMM through LDS): the fragment of
+//     k-step s is 1536 bytes at s * 1536, lane L's d0..d3 at byte 16L and
+//     d4, d5 at byte 1024 + 8L;
+//   * weight layout (loaded by the GEMM straight into registers): k-steps 2u
+//     and 2u + 1 share 3072 bytes at u * 3072, three planes of 1 KiB; lane L's
+//     16 bytes of plane i are at 1024i + 16L, and its 48 bytes in plane order
+//     are the six dwords of k-step 2u followed by those of k-step 2u + 1.
+//     A wave thus loads two k-steps of a band with three 16-byte accesses per
+//     lane (the vector memory path costs about the same per instruction
+//     whatever its width).
 //
-// GEMM structure.  Block tile 256 (m) x 256 (n), one block per CU, four waves,
-// one per SIMD.  Wave w owns weight rows 64w .. 64w+63 of the tile (two bands)
-// and every activation row: 2 x 8 tiles of 32x32, i.e. 256 fp32 accumulators
-// per lane, which gfx950 holds in its accumulation registers beside 256
-// ordinary VGPRs.
-//   * Activations: shared by the four waves, staged through LDS.  A stage is
-//     128 codes of K (two k-steps x eight bands = 16 fragments, 24 KiB), moved
-//     from global memory by buffer_load ... lds (no registers) into a ring of
-//     three stage slots, three stages ahead.
-//   * Weights: private to a wave, loaded straight into registers two stages
-//     ahead (a ring of three register sets, so the stage loop is unrolled by 3).
-//   * Per stage: the sixteen activation fragments roll through a window of
-//     four registers sets (fragment i is read while the MFMAs of fragment
-//     i - 4 run).  Half-way through the stage the wave waits for its share of
-//     the next stage's DMA, meets the others at a barrier (no memory fence),
-//     and issues the weight loads and DMA of the stages ahead.  No VALU work
-//     sits between the MFMAs.
+// GEMM structure.  Block tile (32 * tile_bands) m x 256 n with tile_bands 7
+// or 8, picked per shape to spread the tiles evenly over the CUs; eight
+// waves, two per SIMD, one block per CU, persistent over the tiles in an
+// XCD-aware order.  Wave (wm, wn) owns weight bands 2wn, 2wn + 1 of the tile
+// and the activation bands of half wm (four bands, or tile_bands - 4 in the
+// second half; the two waves on a SIMD belong to different halves, so every
+// SIMD gets the same work): up to 2 x 4 tiles of 32x32, 128 fp32
+// accumulators per lane.
+//   * Activations: shared by the four waves of a half, staged through LDS.  A
+//     stage is 128 codes of K (two k-steps x eight bands = 16 fragments, 24
+//     KiB), moved by buffer_load ... lds (no registers) into a ring of three
+//     stage slots, three stages ahead.
+//   * Weights: loaded straight into registers one stage ahead, two register
+//     sets (so the stage loop is unrolled by six, a multiple of both ring
+//     sizes).
+//   * Per stage: the eight MFMAs of k-step 0 run while the wave reads its
+//     k-step 1 fragments from LDS; then it waits for its share of the next
+//     stage's DMA, meets the others at a barrier (no memory fence) and issues
+//     the DMA three stages ahead into the slot just read; then the MFMAs of
+//     k-step 1 run while the next stage's k-step 0 fragments are read.  No
+//     VALU work sits between the MFMAs.
 //   * The weight fragment is operand A and the activation fragment operand B,
 //     so the 32x32 result is y^T: lane L holds column m = L % 32 and rows
-//     n = 8j + 4(L / 32) + r (j, r = 0..3), i.e. four consecutive outputs of
-//     one row per j, stored as one 8-byte bf16 write.
+//     n = 8j + 4(L / 32) + r (j, r = 0..3).  The epilogue scales them, packs
+//     bf16 and stages them through LDS to store whole 128-byte rows.
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -131,13 +141,26 @@ __device__ __forceinline__ void codes32(const uint32_t* w, float s, float rcp, b
   }
 }
 
-// Store the BF6 group gi (= 2 * kstep + half) of row `row` into the operand layout.
+// Store the BF6 group gi (= 2 * kstep + half) of row `row` into the
+// activation layout (WLAYOUT false) or the weight layout (true).
+template <bool WLAYOUT>
 __device__ __forceinline__ void store_group(uint8_t* out, int64_t ksteps, int64_t row, int gi, v6u d) {
   const int s = gi >> 1, h = gi & 1;
   const int L = static_cast<int>(row & 31) + 32 * h;
-  uint8_t* p = out + ((row >> 5) * ksteps + s) * kFragBytes;
-  *reinterpret_cast<uint4*>(p + 16 * L) = make_uint4(d[0], d[1], d[2], d[3]);
-  *reinterpret_cast<uint2*>(p + 1024 + 8 * L) = make_uint2(d[4], d[5]);
+  if constexpr (!WLAYOUT) {
+    uint8_t* p = out + ((row >> 5) * ksteps + s) * kFragBytes;
+    *reinterpret_cast<uint4*>(p + 16 * L) = make_uint4(d[0], d[1], d[2], d[3]);
+    *reinterpret_cast<uint2*>(p + 1024 + 8 * L) = make_uint2(d[4], d[5]);
+  } else {
+    uint8_t* p = out + (row >> 5) * ksteps * kFragBytes + (s >> 1) * (2 * kFragBytes) + 16 * L;
+    if ((s & 1) == 0) {
+      *reinterpret_cast<uint4*>(p) = make_uint4(d[0], d[1], d[2], d[3]);
+      *reinterpret_cast<uint2*>(p + 1024) = make_uint2(d[4], d[5]);
+    } else {
+      *reinterpret_cast<uint2*>(p + 1024 + 8) = make_uint2(d[0], d[1]);
+      *reinterpret_cast<uint4*>(p + 2048) = make_uint4(d[2], d[3], d[4], d[5]);
+    }
+  }
 }
 
 // Row of block b.  Blocks are dealt round-robin to the 8 XCDs; the 32 rows of
@@ -214,12 +237,14 @@ __global__ __launch_bounds__(512) void quantize_rows_f6_kernel(const uint16_t* _
                               v[j][3].x, v[j][3].y, v[j][3].z, v[j][3].w};
       codes32(w, s, rcp, exact_row, q);
     }
-    store_group(out, ksteps, row, gi, bf6_group(q));
+    store_group<false>(out, ksteps, row, gi, bf6_group(q));
   }
 }
 
-// Canonical packed int4 codes -> BF6 operand.  One thread per (row, 32-code
-// group) of the padded operand; padding rows and codes are written as zeros.
+// Canonical packed int4 codes -> BF6 operand in the activation or the weight
+// layout.  One thread per (row, 32-code group) of the padded operand; padding
+// rows and codes are written as zeros.
+template <bool WLAYOUT>
 __global__ __launch_bounds__(256) void int4_to_f6_kernel(const uint8_t* __restrict__ q, int64_t rows,
                                                          int64_t rows_padded, int64_t K, int64_t ksteps,
                                                          uint8_t* __restrict__ out) {
@@ -238,7 +263,7 @@ __global__ __launch_bounds__(256) void int4_to_f6_kernel(const uint8_t* __restri
 #pragma unroll
     for (int n = 0; n < 8; ++n)  // nibble n of dword d is code 8d + n (even codes in low nibbles)
       c[8 * d + n] = static_cast<float>(static_cast<int>(w[d] << (28 - 4 * n)) >> 28);
-  store_group(out, ksteps, row, gi, bf6_group(c));
+  store_group<WLAYOUT>(out, ksteps, row, gi, bf6_group(c));
 }
 
 // ---------------------------------------------------------------------------
@@ -256,7 +281,7 @@ __device__ __forceinline__ v8i join(v4i32 a, v2i32 b) { return v8i{a.x, a.y, a.z
 constexpr int kWaitcntBase = (0x7 << 4) | (0xF << 8);  // expcnt, lgkmcnt: no wait
 constexpr int vmcnt_imm(int n) { return kWaitcntBase | (n & 0xF) | ((n >> 4) << 14); }
 constexpr int kLgkm0 = 0xC07F;                          // lgkmcnt(0), vmcnt and expcnt: no wait
-constexpr int kWLoads = 8;                              // weight loads per wave per stage
+constexpr int kWLoads = 6;                              // weight loads per wave per stage
 constexpr uint32_t kOutside = 0x80000000u;              // a buffer offset past every operand
 
 template <Epilogue EPI, bool HAS_BIAS>
@@ -349,13 +374,14 @@ __global__ __launch_bounds__(kF6Threads, 1) void w4a4_f6_gemm_kernel(
 #pragma unroll
     for (int f = 0; f < 2; ++f) {
       const uint32_t wb = static_cast<uint32_t>(min(n0 / 32 + 2 * wn + f, nbands - 1)) * band_bytes;
-#pragma unroll
-      for (int s = 0; s < 2; ++s) {
-        const int so = (2 * st + s) * kFragBytes;
-        const v4i32 a = __builtin_bit_cast(v4i32, __builtin_amdgcn_raw_buffer_load_b128(rsw, wb + 16 * lane, so, 0));
-        const v2i32 b = __builtin_bit_cast(v2i32, __builtin_amdgcn_raw_buffer_load_b64(rsw, wb + 1024 + 8 * lane, so, 0));
-        w.f[s][f] = join(a, b);
-      }
+      const int so = 2 * st * kFragBytes;
+      const v4i32 p0 = __builtin_bit_cast(v4i32, __builtin_amdgcn_raw_buffer_load_b128(rsw, wb + 16 * lane, so, 0));
+      const v4i32 p1 =
+          __builtin_bit_cast(v4i32, __builtin_amdgcn_raw_buffer_load_b128(rsw, wb + 1024 + 16 * lane, so, 0));
+      const v4i32 p2 =
+          __builtin_bit_cast(v4i32, __builtin_amdgcn_raw_buffer_load_b128(rsw, wb + 2048 + 16 * lane, so, 0));
+      w.f[0][f] = v8i{p0.x, p0.y, p0.z, p0.w, p1.x, p1.y, 0, 0};
+      w.f[1][f] = v8i{p1.z, p1.w, p2.x, p2.y, p2.z, p2.w, 0, 0};
     }
   };
   // Scales and bias of the tile at (m0, n0) into LDS: waves 0..3 take a
@@ -690,12 +716,16 @@ hipError_t launch_quantize_rows_f6(const uint16_t* x, int64_t M, int64_t K, uint
   return launch_qf6<4>(x, M, K, ksteps, out, scale, th, st);
 }
 
-hipError_t launch_int4_to_f6(const uint8_t* q, int64_t rows, int64_t K, uint8_t* out, hipStream_t st) {
+hipError_t launch_int4_to_f6(const uint8_t* q, int64_t rows, int64_t K, uint8_t* out, bool weight_layout,
+                             hipStream_t st) {
   const int64_t ksteps = f6_ksteps(K);
   const int64_t rows_padded = (rows + 31) / 32 * 32;
   const int64_t total = rows_padded * 2 * ksteps;
   const dim3 grid(static_cast<unsigned>((total + 255) / 256));
-  hipLaunchKernelGGL(int4_to_f6_kernel, grid, dim3(256), 0, st, q, rows, rows_padded, K, ksteps, out);
+  if (weight_layout)
+    hipLaunchKernelGGL(int4_to_f6_kernel<true>, grid, dim3(256), 0, st, q, rows, rows_padded, K, ksteps, out);
+  else
+    hipLaunchKernelGGL(int4_to_f6_kernel<false>, grid, dim3(256), 0, st, q, rows, rows_padded, K, ksteps, out);
   return hipGetLastError();
 }
 

@@ -44,8 +44,9 @@ hipError_t launch_w4a4g_gemm(Epilogue epi, const uint8_t* qx, const float* sx, i
                              const uint8_t* qw, const float* sw, int64_t N, const uint16_t* bias, void* out,
                              hipStream_t st);
 
-// BF6 engine (6-bit MFMA operands).  Both operands use one fragment-major
-// layout of f6_operand_bytes(rows, K) bytes (rows padded to 32, K to 128).
+// BF6 engine (6-bit MFMA operands).  Activations and weights take
+// f6_operand_bytes(rows, K) bytes each (rows padded to 32, K to 128), in the
+// activation layout and the weight layout respectively.
 int64_t f6_ksteps(int64_t K);
 int64_t f6_operand_bytes(int64_t rows, int64_t K);
 // GEMM tile height in bands of 32 rows (7 or 8) for an M x N output on `slots` CUs.
@@ -55,10 +56,13 @@ int f6_tile_bands(int64_t M, int64_t N, int64_t slots);
 hipError_t launch_quantize_rows_f6(const uint16_t* x, int64_t M, int64_t K, uint8_t* out, float* scale,
                                    hipStream_t st);
 
-// Canonical packed int4 codes -> BF6 operand (padding written as zeros).
-hipError_t launch_int4_to_f6(const uint8_t* q, int64_t rows, int64_t K, uint8_t* out, hipStream_t st);
+// Canonical packed int4 codes -> BF6 operand in the activation layout or the
+// weight layout (padding written as zeros).
+hipError_t launch_int4_to_f6(const uint8_t* q, int64_t rows, int64_t K, uint8_t* out, bool weight_layout,
+                             hipStream_t st);
 
-// GEMM on BF6 operands; epi is kBf16 (y = bf16(((acc*sx)*sw)+bias)) or kInt32 (acc).
+// GEMM on BF6 operands (xf6 in the activation layout, wf6 in the weight
+// layout); epi is kBf16 (y = bf16(((acc*sx)*sw)+bias)) or kInt32 (acc).
 hipError_t launch_w4a4_f6_gemm(Epilogue epi, const uint8_t* xf6, const float* sx, int64_t M, int64_t K,
                                const uint8_t* wf6, const float* sw, int64_t N, const uint16_t* bias, void* out,
                                hipStream_t st);

@@ -71,6 +71,21 @@ def decode_f6(buf, rows, K):
     return codes
 
 
+def decode_f6_weight(buf, rows, K):
+    """BF6 operand bytes in the weight layout -> integer codes, as decode_f6."""
+    KS = 2 * ((K + 127) // 128)
+    NB = (rows + 31) // 32
+    blk = np.asarray(buf, np.uint8).reshape(NB, KS // 2, 3, 64, 16)              # [b, u, plane, L, 16]
+    lane = blk.transpose(0, 1, 3, 2, 4).reshape(NB, KS // 2, 64, 48)              # 48 bytes per lane
+    lane = lane.reshape(NB, KS // 2, 64, 2, 24).transpose(0, 1, 3, 2, 4)          # [b, u, t, L, 24]
+    bits = np.unpackbits(lane, axis=4, bitorder="little").reshape(NB, KS // 2, 2, 64, 32, 6)
+    fields = (bits * (1 << np.arange(6))).sum(axis=5)
+    vals = E3M2[fields]
+    assert np.all(vals == np.round(vals)), "non-integer BF6 value"
+    codes = vals.astype(np.int64).reshape(NB, KS, 2, 32, 32)                      # k-step s = 2u + t
+    return codes.transpose(0, 3, 1, 2, 4).reshape(NB * 32, KS * 64)
+
+
 def padded_codes(packed, rows, K):
     c = oracle.unpack_int4(packed).astype(np.int64)
     out = np.zeros((32 * ((rows + 31) // 32), 128 * ((K + 127) // 128)), np.int64)
@@ -132,6 +147,26 @@ def test_decoder_hand_built_fragment():
     assert not dec.any()
 
 
+def test_weight_decoder_hand_built_pair():
+    # weight layout, one band, K = 256: k-step 3 = the second k-step of pair
+    # u = 1; lane 37 = row 5, half 1: codes 3*64 + 32 .. +31 of row 5
+    enc = {0: 0x00, 1: 0x0C, 2: 0x10, 3: 0x12, 4: 0x14, 5: 0x15, 6: 0x16, 7: 0x17, 8: 0x18}
+    codes = [7 - (p % 16) for p in range(32)]
+    word = 0
+    for p, c in enumerate(codes):
+        word |= (enc[abs(c)] | (0x20 if c < 0 else 0)) << (6 * p)
+    d = word.to_bytes(24, "little")             # dwords d0..d5 of the group
+    buf = np.zeros(4 * 1536, np.uint8)
+    base, L = 3072, 37
+    # lane bytes 24..47 of the pair record: the last 8 bytes of plane 1, all of plane 2
+    buf[base + 1024 + 16 * L + 8: base + 1024 + 16 * L + 16] = np.frombuffer(d[:8], np.uint8)
+    buf[base + 2048 + 16 * L: base + 2048 + 16 * L + 16] = np.frombuffer(d[8:], np.uint8)
+    dec = decode_f6_weight(buf, 32, 256)
+    assert dec[5, 224:256].tolist() == codes
+    dec[5, 224:256] = 0
+    assert not dec.any()
+
+
 # ---------------------------------------------------------------------------
 # quantiser and converter
 # ---------------------------------------------------------------------------
@@ -166,6 +201,14 @@ def test_int4_to_f6_lossless(rows, K):
     assert np.array_equal(decode_f6(f6.cpu().numpy(), rows, K), padded_codes(q, rows, K))
 
 
+@pytest.mark.parametrize("rows,K", [(1, 64), (31, 128), (33, 192), (100, 4160), (64, 12288)])
+def test_int4_to_f6_weight_lossless(rows, K):
+    q = rand_packed(rows, K, seed=rows * 5 + K)
+    f6 = jq.jq_int4_to_f6_weight(torch.from_numpy(q).cuda())
+    torch.cuda.synchronize()
+    assert np.array_equal(decode_f6_weight(f6.cpu().numpy(), rows, K), padded_codes(q, rows, K))
+
+
 # ---------------------------------------------------------------------------
 # exact accumulators
 # ---------------------------------------------------------------------------
@@ -174,7 +217,7 @@ def test_int4_to_f6_lossless(rows, K):
 def f6_i32(qx, qw):
     M, N, K = qx.shape[0], qw.shape[0], 2 * qx.shape[1]
     xf6 = jq.jq_int4_to_f6(torch.from_numpy(qx).cuda())
-    wf6 = jq.jq_int4_to_f6(torch.from_numpy(qw).cuda())
+    wf6 = jq.jq_int4_to_f6_weight(torch.from_numpy(qw).cuda())
     acc = jq.jq_w4a4_f6_gemm_i32(xf6, M, K, wf6, N)
     torch.cuda.synchronize()
     return acc.cpu().numpy()
@@ -237,7 +280,7 @@ def test_f6_gemm_i32_large_partial_sums_then_small_terms():
 def f6_layer(bits_x, bits_w, bits_b):
     x = dev_bf16(bits_x)
     wq, sw = jq.jq_pack_weight_int4(dev_bf16(bits_w))
-    wf6 = jq.jq_int4_to_f6(wq)
+    wf6 = jq.jq_int4_to_f6_weight(wq)
     b = None if bits_b is None else dev_bf16(bits_b)
     y = jq.jq_w4a4_f6_linear(x, wf6, sw, b)
     torch.cuda.synchronize()
@@ -281,7 +324,7 @@ def test_f6_gemm_matches_linear():
     M = 512
     x = dev_bf16(lin.make_x()[:M])
     wq, sw = jq.jq_pack_weight_int4(dev_bf16(lin.make_w()[:1024]))
-    wf6 = jq.jq_int4_to_f6(wq)
+    wf6 = jq.jq_int4_to_f6_weight(wq)
     xf6, s = jq.jq_quantize_act_f6(x)
     y1 = jq.jq_w4a4_f6_gemm(xf6, s, lin.K, wf6, sw)
     y2 = jq.jq_w4a4_f6_linear(x, wf6, sw)
@@ -304,7 +347,7 @@ def test_f6_linear_full_size(lin):
     x_bits, w_bits, b_bits = lin.make_x(), lin.make_w(), lin.make_bias()
     x = dev_bf16(x_bits)
     wq, sw = jq.jq_pack_weight_int4(dev_bf16(w_bits))
-    wf6 = jq.jq_int4_to_f6(wq)
+    wf6 = jq.jq_int4_to_f6_weight(wq)
     b = None if b_bits is None else dev_bf16(b_bits)
     y6 = jq.jq_w4a4_f6_linear(x, wf6, sw, b)
     y4 = jq.jq_w4a4_linear(x, wq, sw, b)
