@@ -112,32 +112,44 @@ constexpr float kNearTie = 0.5f - 0x1p-17f;
 __device__ __forceinline__ float bf16_lo(uint32_t u) { return __uint_as_float(u << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t u) { return __uint_as_float(u & 0xFFFF0000u); }
 
-// Codes of one 32-element group (16 dwords of bf16 pairs).  Reciprocal path
-// with the exact IEEE division wherever the product sits next to a rounding
-// decision point (the argument is that of the packed-int4 quantiser), or the
-// division for every element when the reciprocal overflows.
-__device__ __forceinline__ void codes32(const uint32_t* w, float s, float rcp, bool exact_row, float* q) {
-  bool near = exact_row;
-  if (!exact_row) {
-    float dmax = 0.0f;
+// Codes of one 32-element group (16 dwords of bf16 pairs): the reciprocal
+// products rounded, unless one of them sits next to a rounding decision point
+// or the reciprocal overflows (the argument is that of the packed-int4
+// quantiser); then every code of the group is the exact IEEE quotient.  That
+// rare path reloads the inputs through `reload`, so the common path need not
+// keep them in registers.
+template <typename Reload>
+__device__ __forceinline__ void codes32(const uint32_t* w, float s, float rcp, bool exact_row, float* q,
+                                        Reload reload) {
+  float dmax = 0.0f;
 #pragma unroll
-    for (int j = 0; j < 16; ++j) {
-      const float te = bf16_lo(w[j]) * rcp;
-      const float to = bf16_hi(w[j]) * rcp;
-      const float re = (te + kMagic) - kMagic;
-      const float ro = (to + kMagic) - kMagic;
-      dmax = fmaxf(dmax, fmaxf(fabsf(te - re), fabsf(to - ro)));
-      q[2 * j] = re;
-      q[2 * j + 1] = ro;
-    }
-    near = !(dmax < kNearTie);
+  for (int j = 0; j < 16; ++j) {
+    const float te = bf16_lo(w[j]) * rcp;
+    const float to = bf16_hi(w[j]) * rcp;
+    const float re = (te + kMagic) - kMagic;
+    const float ro = (to + kMagic) - kMagic;
+    dmax = fmaxf(dmax, fmaxf(fabsf(te - re), fabsf(to - ro)));
+    q[2 * j] = re;
+    q[2 * j + 1] = ro;
   }
-  if (near) {
+  if (exact_row || !(dmax < kNearTie)) {
+    uint32_t u[16];
+    reload(u);
 #pragma unroll
     for (int j = 0; j < 16; ++j) {
-      q[2 * j] = fminf(fmaxf(__builtin_rintf(bf16_lo(w[j]) / s), -8.0f), 7.0f);
-      q[2 * j + 1] = fminf(fmaxf(__builtin_rintf(bf16_hi(w[j]) / s), -8.0f), 7.0f);
+      q[2 * j] = fminf(fmaxf(__builtin_rintf(bf16_lo(u[j]) / s), -8.0f), 7.0f);
+      q[2 * j + 1] = fminf(fmaxf(__builtin_rintf(bf16_hi(u[j]) / s), -8.0f), 7.0f);
     }
+  }
+}
+
+// The 16 dwords of bf16 pairs of the group at element k of row xr (zeros past
+// the row or for a padding row).
+__device__ __forceinline__ void load_group(const uint16_t* xr, bool live, int64_t k, int64_t K, uint32_t* u) {
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    const uint4 t = (live && k < K) ? *reinterpret_cast<const uint4*>(xr + k + 8 * c) : make_uint4(0, 0, 0, 0);
+    u[4 * c] = t.x, u[4 * c + 1] = t.y, u[4 * c + 2] = t.z, u[4 * c + 3] = t.w;
   }
 }
 
@@ -235,7 +247,8 @@ __global__ __launch_bounds__(512) void quantize_rows_f6_kernel(const uint16_t* _
       const uint32_t w[16] = {v[j][0].x, v[j][0].y, v[j][0].z, v[j][0].w, v[j][1].x, v[j][1].y,
                               v[j][1].z, v[j][1].w, v[j][2].x, v[j][2].y, v[j][2].z, v[j][2].w,
                               v[j][3].x, v[j][3].y, v[j][3].z, v[j][3].w};
-      codes32(w, s, rcp, exact_row, q);
+      codes32(w, s, rcp, exact_row, q,
+              [&](uint32_t* u) { load_group(xr, live, 32 * static_cast<int64_t>(gi), K, u); });
     }
     store_group<false>(out, ksteps, row, gi, bf6_group(q));
   }
@@ -270,6 +283,8 @@ __global__ __launch_bounds__(256) void int4_to_f6_kernel(const uint8_t* __restri
 // GEMM
 
 typedef int v4i32 __attribute__((ext_vector_type(4)));
+typedef unsigned v4u32 __attribute__((ext_vector_type(4)));
+typedef unsigned v2u32 __attribute__((ext_vector_type(2)));
 typedef int v2i32 __attribute__((ext_vector_type(2)));
 
 struct WFrag {
@@ -297,12 +312,15 @@ __global__ __launch_bounds__(kF6Threads, 1) void w4a4_f6_gemm_kernel(
   __shared__ uint4 lds1[kStageU4];
   __shared__ uint4 lds2[kStageU4];
   // Output staging for the epilogue: per wave 64 rows x 64 bf16 (128 bytes a
-  // row), 16-byte chunk c of row r at chunk c ^ ((r >> 1) & 7).
-  __shared__ uint4 stg[kF6Threads / 64][512];
+  // row), 16-byte chunk c of row r at chunk c ^ ((r >> 1) & 7).  Accessed
+  // only as stg[i] / stg2[i] with a computed index, so that every access
+  // keeps the alias information that tells it apart from the DMA targets
+  // (an access without it would wait for every load in flight).
+  __shared__ v4u32 stg[kF6Threads / 64 * 512];
   // The current tile's scales and bias, moved in by DMA for the epilogue.
   __shared__ float sc_x[kFBM];
   __shared__ float sc_w[kFBN];
-  __shared__ uint32_t sc_b[kFBN / 2];
+  __shared__ float sc_b[kFBN / 2];  // bf16 pairs
   auto slot = [&](int k) __attribute__((always_inline)) { return k == 0 ? lds0 : (k == 1 ? lds1 : lds2); };
 
   const int tid = threadIdx.x;
@@ -402,7 +420,7 @@ __global__ __launch_bounds__(kF6Threads, 1) void w4a4_f6_gemm_kernel(
       if (HAS_BIAS && wave < 2) {
         const __amdgpu_buffer_rsrc_t r =
             __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(bias), 0, 2 * N, kBufferFlags);
-        dma4(r, reinterpret_cast<float*>(sc_b + 64 * wave), 2 * static_cast<uint32_t>(n0 + 128 * wave + 2 * lane), 0);
+        dma4(r, sc_b + 64 * wave, 2 * static_cast<uint32_t>(n0 + 128 * wave + 2 * lane), 0);
       }
     }
   };
@@ -508,7 +526,8 @@ __global__ __launch_bounds__(kF6Threads, 1) void w4a4_f6_gemm_kernel(
       // memory as whole 128-byte rows, eight rows per instruction (in a ragged
       // tile, element by element where a row runs past M or N).
       uint16_t* o = static_cast<uint16_t*>(out);
-      uint8_t* sb = reinterpret_cast<uint8_t*>(stg[wave]);
+      v2u32* stg2 = reinterpret_cast<v2u32*>(stg);
+      const int sbase = 512 * wave;  // the wave's area, in 16-byte units
       const bool vec = full && (N % 8 == 0);
 #pragma unroll
       for (int ph = 0; ph < 2; ++ph) {
@@ -523,17 +542,22 @@ __global__ __launch_bounds__(kF6Threads, 1) void w4a4_f6_gemm_kernel(
             float bv[4] = {0.0f, 0.0f, 0.0f, 0.0f};
             if (HAS_BIAS) {
               if (full) {
-                const uint2 bb = *reinterpret_cast<const uint2*>(sc_b + c / 2);
-                bv[0] = __uint_as_float(bb.x << 16);
-                bv[1] = __uint_as_float(bb.x & 0xFFFF0000u);
-                bv[2] = __uint_as_float(bb.y << 16);
-                bv[3] = __uint_as_float(bb.y & 0xFFFF0000u);
+                const float2 bf = *reinterpret_cast<const float2*>(sc_b + c / 2);
+                const uint32_t b0 = __float_as_uint(bf.x), b1 = __float_as_uint(bf.y);
+                bv[0] = __uint_as_float(b0 << 16);
+                bv[1] = __uint_as_float(b0 & 0xFFFF0000u);
+                bv[2] = __uint_as_float(b1 << 16);
+                bv[3] = __uint_as_float(b1 & 0xFFFF0000u);
               } else {
                 // a ragged tile (with odd N the last staged pair of bias values
                 // reads past the buffer as zero): straight from memory
 #pragma unroll
                 for (int r = 0; r < 4; ++r)
                   bv[r] = __uint_as_float(static_cast<uint32_t>(bias[min(cn0 + c + r, N - 1)]) << 16);
+                // settle these loads here, in the ragged branch: otherwise the
+                // wait for them lands after the branches join and, in every
+                // tile, waits for all the prefetches in flight
+                __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
               }
             }
 #pragma unroll
@@ -552,8 +576,8 @@ __global__ __launch_bounds__(kF6Threads, 1) void w4a4_f6_gemm_kernel(
               const int row = 32 * fh + (lane & 31);
               const int col = c - 64 * wn;  // within the wave's 64 columns
               const int chunk = (col >> 3) ^ ((row >> 1) & 7);
-              *reinterpret_cast<uint2*>(sb + 128 * row + 16 * chunk + 2 * (col & 7)) =
-                  make_uint2(h[0] | (static_cast<uint32_t>(h[1]) << 16), h[2] | (static_cast<uint32_t>(h[3]) << 16));
+              stg2[2 * (sbase + 8 * row + chunk) + ((col & 7) >> 2)] =
+                  v2u32{h[0] | (static_cast<uint32_t>(h[1]) << 16), h[2] | (static_cast<uint32_t>(h[3]) << 16)};
             }
           }
         __builtin_amdgcn_wave_barrier();
@@ -561,7 +585,8 @@ __global__ __launch_bounds__(kF6Threads, 1) void w4a4_f6_gemm_kernel(
         for (int it = 0; it < 8; ++it) {
           const int row = 8 * it + (lane >> 3);
           const int c = lane & 7;
-          const uint4 v = *reinterpret_cast<const uint4*>(sb + 128 * row + 16 * (c ^ ((row >> 1) & 7)));
+          const v4u32 vv = stg[sbase + 8 * row + (c ^ ((row >> 1) & 7))];
+          const uint4 v = make_uint4(vv.x, vv.y, vv.z, vv.w);
           const int m = cm0 + 128 * wm + 64 * ph + row;
           const int n = cn0 + 64 * wn + 8 * c;
           uint16_t* p = o + static_cast<int64_t>(m) * N + n;
