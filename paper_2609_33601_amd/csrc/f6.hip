@@ -106,14 +106,15 @@ __device__ __forceinline__ v6u bf6_group(const float* q) {
   return __builtin_amdgcn_cvt_scalef32_2xpk16_bf6_f32(ev, od, 1.0f);
 }
 
-constexpr float kMagic = 12582912.0f;         // 1.5 * 2^23
 constexpr float kNearTie = 0.5f - 0x1p-17f;
 
 __device__ __forceinline__ float bf16_lo(uint32_t u) { return __uint_as_float(u << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t u) { return __uint_as_float(u & 0xFFFF0000u); }
 
 // Codes of one 32-element group (16 dwords of bf16 pairs): the reciprocal
-// products rounded, unless one of them sits next to a rounding decision point
+// products rounded (a zero code keeps the sign of its input, which the BF6
+// encoding carries in its sign bit: both are zero), unless one of them sits
+// next to a rounding decision point
 // or the reciprocal overflows (the argument is that of the packed-int4
 // quantiser); then every code of the group is the exact IEEE quotient.  That
 // rare path reloads the inputs through `reload`, so the common path need not
@@ -126,8 +127,8 @@ __device__ __forceinline__ void codes32(const uint32_t* w, float s, float rcp, b
   for (int j = 0; j < 16; ++j) {
     const float te = bf16_lo(w[j]) * rcp;
     const float to = bf16_hi(w[j]) * rcp;
-    const float re = (te + kMagic) - kMagic;
-    const float ro = (to + kMagic) - kMagic;
+    const float re = __builtin_rintf(te);
+    const float ro = __builtin_rintf(to);
     dmax = fmaxf(dmax, fmaxf(fabsf(te - re), fabsf(to - ro)));
     q[2 * j] = re;
     q[2 * j + 1] = ro;
