@@ -64,6 +64,9 @@ namespace {
 
 using namespace gemm_detail;
 
+typedef unsigned v4u32 __attribute__((ext_vector_type(4)));
+typedef unsigned v2u32 __attribute__((ext_vector_type(2)));
+
 constexpr int kBM = 128;       // activation rows per block
 constexpr int kBN = 256;       // weight rows per block
 constexpr int kXSlots = kBM * kXChunks;      // 16-byte slots of the int8 activation tile
@@ -127,8 +130,10 @@ __global__ __launch_bounds__(kThreads, 2) void w4a4_gemm_kernel(
     const uint16_t* __restrict__ bias, void* __restrict__ out, int tiles_m, int tiles_n) {
   using WT = WTraits<WF>;
   constexpr int kStageSlots = WT::kStageSlots, kWDma = WT::kDma;
-  // Two stage buffers, each the int8 activation tile followed by the packed weight tile.
-  __shared__ uint4 lds[2 * kStageSlots];
+  // Two stage buffers, each the int8 activation tile followed by the packed
+  // weight tile; the bf16 epilogue reuses them to stage the output tile.
+  constexpr int kOutSlots = kThreads / 64 * kWM * kWN * 2 / 16;
+  __shared__ uint4 lds[2 * kStageSlots > kOutSlots ? 2 * kStageSlots : kOutSlots];
 
   TileCoord tc;
   if (!tile_of_block(blockIdx.x, tiles_m, tiles_n, &tc)) return;
@@ -312,6 +317,12 @@ __global__ __launch_bounds__(kThreads, 2) void w4a4_gemm_kernel(
     }
   } else {
     uint16_t* o = static_cast<uint16_t*>(out);
+    // The stage buffers are free once every wave is done with the last
+    // stage; each wave then stages its outputs in 16 KiB of them.
+    __syncthreads();
+    v4u32* stg = reinterpret_cast<v4u32*>(lds);
+    v2u32* stg2 = reinterpret_cast<v2u32*>(lds);
+    const int sbase = wave * (kWM * kWN * 2 / 16);  // in 16-byte units
     float sxv[kFM];
 #pragma unroll
     for (int fm = 0; fm < kFM; ++fm) sxv[fm] = sx[min(mb + 16 * fm, M - 1)];
@@ -327,7 +338,6 @@ __global__ __launch_bounds__(kThreads, 2) void w4a4_gemm_kernel(
       }
 #pragma unroll
       for (int fm = 0; fm < kFM; ++fm) {
-        const int m = mb + 16 * fm;
         const v4i a = acc[fn][fm];
         uint16_t h[4];
 #pragma unroll
@@ -338,15 +348,32 @@ __global__ __launch_bounds__(kThreads, 2) void w4a4_gemm_kernel(
           if (HAS_BIAS) f = f + bv[r];
           h[r] = __builtin_bit_cast(uint16_t, static_cast<__bf16>(f));
         }
-        uint16_t* p = o + static_cast<int64_t>(m) * N + n;
-        if (full) {
-          *reinterpret_cast<uint2*>(p) = make_uint2(h[0] | (static_cast<uint32_t>(h[1]) << 16),
-                                                    h[2] | (static_cast<uint32_t>(h[3]) << 16));
-        } else if (m < M) {
+        // staged in LDS: the wave's 128 rows x 64 columns, 128 bytes a row,
+        // 16-byte chunk c of row rr at chunk c ^ (rr & 7)
+        const int rr = 16 * fm + li, col = 16 * fn + 4 * lg;
+        stg2[2 * (sbase + 8 * rr + ((col >> 3) ^ (rr & 7))) + ((col & 7) >> 2)] =
+            v2u32{h[0] | (static_cast<uint32_t>(h[1]) << 16), h[2] | (static_cast<uint32_t>(h[3]) << 16)};
+      }
+    }
+    __builtin_amdgcn_wave_barrier();
+    // whole 128-byte rows to memory, eight rows per instruction (in a ragged
+    // tile, element by element where a row runs past M or N)
+    const bool vec = full && (N % 8 == 0);
 #pragma unroll
-          for (int r = 0; r < 4; ++r)
-            if (n + r < N) p[r] = h[r];
-        }
+    for (int it = 0; it < kWM / 8; ++it) {
+      const int rr = 8 * it + (lane >> 3), c = lane & 7;
+      const v4u32 v = stg[sbase + 8 * rr + (c ^ (rr & 7))];
+      const int m = m0 + rr;
+      const int n = n0 + kWN * wn + 8 * c;
+      uint16_t* p = o + static_cast<int64_t>(m) * N + n;
+      if (m >= M) {
+      } else if (vec) {
+        *reinterpret_cast<uint4*>(p) = make_uint4(v.x, v.y, v.z, v.w);
+      } else {
+        const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          if (n + e < N) p[e] = static_cast<uint16_t>(w[e >> 1] >> (16 * (e & 1)));
       }
     }
   }
