@@ -106,53 +106,38 @@ __device__ __forceinline__ v6u bf6_group(const float* q) {
   return __builtin_amdgcn_cvt_scalef32_2xpk16_bf6_f32(ev, od, 1.0f);
 }
 
+constexpr float kMagic = 12582912.0f;         // 1.5 * 2^23
 constexpr float kNearTie = 0.5f - 0x1p-17f;
 
 __device__ __forceinline__ float bf16_lo(uint32_t u) { return __uint_as_float(u << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t u) { return __uint_as_float(u & 0xFFFF0000u); }
 
-// BF6 codes of one 32-element group (16 dwords of bf16 pairs; element 2j
-// in the low half of dword j, 2j + 1 in the high half): the reciprocal
-// products rounded (a zero code keeps the sign of its input, which the BF6
-// encoding carries in its sign bit: both are zero), unless one of them sits
-// next to a rounding decision point or the reciprocal overflows (the argument
-// is that of the packed-int4 quantiser); then every code of the group is the
-// exact IEEE quotient.  That rare path reloads the inputs through `reload`,
-// so the common path need not keep them in registers.  The codes go
-// straight into the converter's two sources (even and odd elements).
-template <typename Reload>
-__device__ __forceinline__ v6u codes_bf6(const uint32_t* w, float s, float rcp, bool exact_row, Reload reload) {
-  v16f32 ev, od;
-  float dmax = 0.0f;
-#pragma unroll
-  for (int j = 0; j < 16; ++j) {
-    const float te = bf16_lo(w[j]) * rcp;
-    const float to = bf16_hi(w[j]) * rcp;
-    const float re = __builtin_rintf(te);
-    const float ro = __builtin_rintf(to);
-    dmax = fmaxf(dmax, fmaxf(fabsf(te - re), fabsf(to - ro)));
-    ev[j] = re;
-    od[j] = ro;
-  }
-  if (exact_row || !(dmax < kNearTie)) {
-    uint32_t u[16];
-    reload(u);
+// Codes of one 32-element group (16 dwords of bf16 pairs).  Reciprocal path
+// with the exact IEEE division wherever the product sits next to a rounding
+// decision point (the argument is that of the packed-int4 quantiser), or the
+// division for every element when the reciprocal overflows.
+__device__ __forceinline__ void codes32(const uint32_t* w, float s, float rcp, bool exact_row, float* q) {
+  bool near = exact_row;
+  if (!exact_row) {
+    float dmax = 0.0f;
 #pragma unroll
     for (int j = 0; j < 16; ++j) {
-      ev[j] = fminf(fmaxf(__builtin_rintf(bf16_lo(u[j]) / s), -8.0f), 7.0f);
-      od[j] = fminf(fmaxf(__builtin_rintf(bf16_hi(u[j]) / s), -8.0f), 7.0f);
+      const float te = bf16_lo(w[j]) * rcp;
+      const float to = bf16_hi(w[j]) * rcp;
+      const float re = (te + kMagic) - kMagic;
+      const float ro = (to + kMagic) - kMagic;
+      dmax = fmaxf(dmax, fmaxf(fabsf(te - re), fabsf(to - ro)));
+      q[2 * j] = re;
+      q[2 * j + 1] = ro;
     }
+    near = !(dmax < kNearTie);
   }
-  return __builtin_amdgcn_cvt_scalef32_2xpk16_bf6_f32(ev, od, 1.0f);
-}
-
-// The 16 dwords of bf16 pairs of the group at element k of row xr (zeros past
-// the row or for a padding row).
-__device__ __forceinline__ void load_group(const uint16_t* xr, bool live, int64_t k, int64_t K, uint32_t* u) {
+  if (near) {
 #pragma unroll
-  for (int c = 0; c < 4; ++c) {
-    const uint4 t = (live && k < K) ? *reinterpret_cast<const uint4*>(xr + k + 8 * c) : make_uint4(0, 0, 0, 0);
-    u[4 * c] = t.x, u[4 * c + 1] = t.y, u[4 * c + 2] = t.z, u[4 * c + 3] = t.w;
+    for (int j = 0; j < 16; ++j) {
+      q[2 * j] = fminf(fmaxf(__builtin_rintf(bf16_lo(w[j]) / s), -8.0f), 7.0f);
+      q[2 * j + 1] = fminf(fmaxf(__builtin_rintf(bf16_hi(w[j]) / s), -8.0f), 7.0f);
+    }
   }
 }
 
@@ -242,15 +227,17 @@ __global__ __launch_bounds__(512) void quantize_rows_f6_kernel(const uint16_t* _
   for (int j = 0; j < NJ; ++j) {
     const int gi = threadIdx.x + T * j;
     if (gi >= groups) continue;
-    v6u d = {0, 0, 0, 0, 0, 0};
-    if (s != 0.0f) {
+    float q[32];
+    if (s == 0.0f) {
+#pragma unroll
+      for (int p = 0; p < 32; ++p) q[p] = 0.0f;
+    } else {
       const uint32_t w[16] = {v[j][0].x, v[j][0].y, v[j][0].z, v[j][0].w, v[j][1].x, v[j][1].y,
                               v[j][1].z, v[j][1].w, v[j][2].x, v[j][2].y, v[j][2].z, v[j][2].w,
                               v[j][3].x, v[j][3].y, v[j][3].z, v[j][3].w};
-      d = codes_bf6(w, s, rcp, exact_row,
-                    [&](uint32_t* u) { load_group(xr, live, 32 * static_cast<int64_t>(gi), K, u); });
+      codes32(w, s, rcp, exact_row, q);
     }
-    store_group<false>(out, ksteps, row, gi, d);
+    store_group<false>(out, ksteps, row, gi, bf6_group(q));
   }
 }
 
