@@ -602,9 +602,12 @@ __global__ __launch_bounds__(kF6Threads, 1) void w4a4_f6_gemm_kernel(
   // with at stage g - 1).  Half way through, once every wave has read the
   // whole slot (lgkmcnt(0) + barrier) and DMA(g + 1) has landed, the slot
   // takes the DMA of stage g + 3 (at a tile's first stage, the tile's scales
-  // are moved first).  The wait there, vmcnt(11), leaves in flight exactly
-  // the loads issued since stage g's weights: DMA(g + 2) and stage g + 1's
-  // weights.  After a tile's last stage comes its epilogue.
+  // are moved first).  The wait there, vmcnt(kWLoads + kDmaPerWave) = 9,
+  // leaves in flight at most the loads issued since stage g's weights:
+  // DMA(g + 2) and stage g + 1's weights.  Vector loads complete in order,
+  // so DMA(g + 1), issued before those, has landed (the stores of an
+  // epilogue in between only add to the count).  After a tile's last stage
+  // comes its epilogue.
   WFrag* wset[2] = {&w0, &w1};
   int t = 0, ti = 0;
   auto stage = [&](auto I) __attribute__((always_inline)) {
