@@ -286,7 +286,10 @@ constexpr int kLgkm0 = 0xC07F;                          // lgkmcnt(0), vmcnt and
 constexpr int kWLoads = 6;                              // weight loads per wave per stage
 constexpr uint32_t kOutside = 0x80000000u;              // a buffer offset past every operand
 
-template <Epilogue EPI, bool HAS_BIAS>
+// BIAS_TAIL: a bias with odd N, whose last value the epilogue of a ragged
+// tile reads from memory (its staged pair reads past the buffer as zero);
+// otherwise every bias value comes from LDS and the epilogue has no branch.
+template <Epilogue EPI, bool HAS_BIAS, bool BIAS_TAIL>
 __global__ __launch_bounds__(kF6Threads, 1) void w4a4_f6_gemm_kernel(
     const uint8_t* __restrict__ xf6, const float* __restrict__ sx, int M, int mbands,
     const uint8_t* __restrict__ wf6, const float* __restrict__ sw, int N, int nbands, int ksteps,
@@ -528,7 +531,7 @@ __global__ __launch_bounds__(kF6Threads, 1) void w4a4_f6_gemm_kernel(
             const float swa[4] = {swv.x, swv.y, swv.z, swv.w};
             float bv[4] = {0.0f, 0.0f, 0.0f, 0.0f};
             if (HAS_BIAS) {
-              if (full) {
+              if (!BIAS_TAIL || full) {
                 const float2 bf = *reinterpret_cast<const float2*>(sc_b + c / 2);
                 const uint32_t b0 = __float_as_uint(bf.x), b1 = __float_as_uint(bf.y);
                 bv[0] = __uint_as_float(b0 << 16);
@@ -765,12 +768,13 @@ hipError_t launch_w4a4_f6_gemm(Epilogue epi, const uint8_t* xf6, const float* sx
   const int mbands = static_cast<int>((M + 31) / 32);
   const int nbands = static_cast<int>((N + 31) / 32);
   const int Mi = static_cast<int>(M), Ni = static_cast<int>(N);
-#define JQ_F6(E, B)                                                                                     \
-  hipLaunchKernelGGL((w4a4_f6_gemm_kernel<E, B>), dim3(blocks), dim3(kF6Threads), 0, st, xf6, sx, Mi, mbands, \
+#define JQ_F6(E, B, BT)                                                                                  \
+  hipLaunchKernelGGL((w4a4_f6_gemm_kernel<E, B, BT>), dim3(blocks), dim3(kF6Threads), 0, st, xf6, sx, Mi, mbands, \
                      wf6, sw, Ni, nbands, ksteps, bias, out, tile_bands, tiles_m, tiles_n, blocks)
-  if (epi == Epilogue::kInt32) JQ_F6(Epilogue::kInt32, false);
-  else if (bias != nullptr) JQ_F6(Epilogue::kBf16, true);
-  else JQ_F6(Epilogue::kBf16, false);
+  if (epi == Epilogue::kInt32) JQ_F6(Epilogue::kInt32, false, false);
+  else if (bias != nullptr && (N & 1)) JQ_F6(Epilogue::kBf16, true, true);
+  else if (bias != nullptr) JQ_F6(Epilogue::kBf16, true, false);
+  else JQ_F6(Epilogue::kBf16, false, false);
 #undef JQ_F6
   return hipGetLastError();
 }
