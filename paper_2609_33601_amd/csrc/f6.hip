@@ -38,18 +38,28 @@
 //     lane (the vector memory path costs about the same per instruction
 //     whatever its width).
 //
-// GEMM structure.  Block tile (32 * tile_bands) m x 256 n with tile_bands 7
-// or 8, picked per shape to spread the tiles evenly over the CUs; eight
-// waves, two per SIMD, one block per CU, persistent over the tiles in an
-// XCD-aware order.  Wave (wm, wn) owns weight bands 2wn, 2wn + 1 of the tile
-// and the activation bands of half wm (four bands, or tile_bands - 4 in the
-// second half; the two waves on a SIMD belong to different halves, so every
-// SIMD gets the same work): up to 2 x 4 tiles of 32x32, 128 fp32
-// accumulators per lane.
-//   * Activations: shared by the four waves of a half, staged through LDS.  A
-//     stage is 128 codes of K (two k-steps x eight bands = 16 fragments, 24
-//     KiB), moved by buffer_load ... lds (no registers) into a ring of three
-//     stage slots, three stages ahead.
+// GEMM structure.  Persistent blocks walk the output tiles (256 n columns
+// each) in an XCD-aware order, in one of two shapes:
+//   * one 8-wave block per CU (two waves per SIMD) on tiles of
+//     32 * tile_bands rows, tile_bands 7 or 8 picked per shape to spread the
+//     tiles evenly over the CUs.  Wave (wm, wn) owns weight bands 2wn,
+//     2wn + 1 of the tile and the activation bands of half wm (four bands,
+//     or tile_bands - 4 in the second half; the two waves on a SIMD belong
+//     to different halves, so every SIMD gets the same work);
+//   * two 4-wave blocks per CU on tiles of 128 rows, wave wn owning weight
+//     bands 2wn, 2wn + 1 and all four activation bands.  Taken where 256-row
+//     tiles would not cover M evenly and K is not long: each block's epilogue
+//     then runs beside the other block's MFMAs.  So that the two blocks of a
+//     CU stay out of step, the blocks in the second half of each XCD's share
+//     walk K from its middle stage round to it (the sum is exact in any
+//     order).
+// Either way a wave holds up to 2 x 4 tiles of 32x32, 128 fp32 accumulators
+// per lane.
+//   * Activations: shared by the four waves that read the same bands, staged
+//     through LDS.  A stage is 128 codes of K (two k-steps x the block's
+//     activation bands: 16 fragments, 24 KiB, or 8 fragments, 12 KiB),
+//     moved by buffer_load ... lds (no registers) into a ring of three stage
+//     slots, three stages ahead.
 //   * Weights: loaded straight into registers one stage ahead, two register
 //     sets (so the stage loop is unrolled by six, a multiple of both ring
 //     sizes).
@@ -86,13 +96,23 @@ typedef float v16f32 __attribute__((ext_vector_type(16)));
 typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
 
 constexpr int kFragBytes = 1536;          // one 32-row x 64-code fragment
-constexpr int kFBM = 256, kFBN = 256;     // block tile
-constexpr int kStageBytes = 2 * 8 * kFragBytes;      // 24 KiB: two k-steps x eight bands
-constexpr int kStageU4 = kStageBytes / 16;
-constexpr int kF6Threads = 512;                       // eight waves, two per SIMD
-constexpr int kDmaPerWave = kStageU4 / 64 / (kF6Threads / 64);  // 3 DMA instructions per wave per stage
+constexpr int kFBN = 256;                 // block tile columns
+constexpr int kDmaPerWave = 3;            // stage DMA instructions per wave
+constexpr int64_t kShortK = 6144;          // largest K that may take the two-block shape
 
-static_assert(kDmaPerWave == 3, "stage DMA split assumes 3 instructions per wave");
+// The GEMM comes in two block shapes (WAVES = 8 or 4 waves of 64): one
+// 8-wave block per CU on a tile of up to 256 activation rows, or two 4-wave
+// blocks per CU on tiles of 128 rows.  Per wave the work is the same (two
+// weight bands, four activation bands); a stage holds the block's
+// activation bands for two k-steps.
+template <int WAVES>
+struct F6Shape {
+  static constexpr int kThreads = 64 * WAVES;
+  static constexpr int kBands = WAVES;                          // activation bands staged per tile
+  static constexpr int kFBM = 32 * kBands;                      // tile rows at most
+  static constexpr int kStageU4 = 2 * kBands * kFragBytes / 16;  // one stage slot, 16-byte units
+  static_assert(kStageU4 == 64 * kDmaPerWave * WAVES, "a stage is 3 DMA instructions per wave");
+};
 
 // 32 codes (as exact fp32 integers, code p in q[p]) -> six dwords, code p in bits 6p..6p+5.
 // The converter interleaves its two sources (field 2i <- src0[i], field 2i+1 <- src1[i]).
@@ -289,15 +309,17 @@ constexpr uint32_t kOutside = 0x80000000u;              // a buffer offset past 
 // BIAS_TAIL: a bias with odd N, whose last value the epilogue of a ragged
 // tile reads from memory (its staged pair reads past the buffer as zero);
 // otherwise every bias value comes from LDS and the epilogue has no branch.
-template <Epilogue EPI, bool HAS_BIAS, bool BIAS_TAIL>
-__global__ __launch_bounds__(kF6Threads, 1) void w4a4_f6_gemm_kernel(
+template <int WAVES, Epilogue EPI, bool HAS_BIAS, bool BIAS_TAIL>
+__global__ __launch_bounds__(64 * WAVES, 8 / WAVES) void w4a4_f6_gemm_kernel(
     const uint8_t* __restrict__ xf6, const float* __restrict__ sx, int M, int mbands,
     const uint8_t* __restrict__ wf6, const float* __restrict__ sw, int N, int nbands, int ksteps,
     const uint16_t* __restrict__ bias, void* __restrict__ out, int tile_bands, int tiles_m, int tiles_n,
     int grid_blocks) {
-  // The 72 KiB ring as three separate arrays.  With the stage loop
+  // The ring (72 or 36 KiB) as three separate arrays.  With the stage loop
   // unrolled by six every slot is known at compile time, so the compiler
   // can tell the slot being read from the one the DMA is writing.
+  using S = F6Shape<WAVES>;
+  constexpr int kStageU4 = S::kStageU4, kFBM = S::kFBM, kF6Threads = S::kThreads;
   __shared__ uint4 lds0[kStageU4];
   __shared__ uint4 lds1[kStageU4];
   __shared__ uint4 lds2[kStageU4];
@@ -316,7 +338,7 @@ __global__ __launch_bounds__(kF6Threads, 1) void w4a4_f6_gemm_kernel(
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wm = wave >> 2, wn = wave & 3;  // activation half, weight quarter (2 bands)
+  const int wm = WAVES == 8 ? wave >> 2 : 0, wn = wave & 3;  // activation half, weight quarter (2 bands)
   // A tile has tile_bands (7 or 8) bands of 32 activation rows: the first
   // half takes four of them, the second half the rest, so each SIMD (one wave
   // of each half) does the same work whatever the tile height.
@@ -364,10 +386,18 @@ __global__ __launch_bounds__(kF6Threads, 1) void w4a4_f6_gemm_kernel(
   for (int j = 0; j < kDmaPerWave; ++j) {
     const int Q = 64 * (kDmaPerWave * wave + j) + lane;
     const int R = Q / 96, q = Q % 96;
-    rband[j] = R & 7;
-    rpart[j] = (R & 7) < tile_bands ? (R >> 3) * kFragBytes + 16 * q : kOutside;
+    rband[j] = R % S::kBands;
+    rpart[j] = (R % S::kBands) < tile_bands ? (R / S::kBands) * kFragBytes + 16 * q : kOutside;
   }
   const uint32_t band_bytes = static_cast<uint32_t>(ksteps) * kFragBytes;
+  // With two blocks per CU, the second half of each XCD's blocks walks the
+  // stages of its tiles from the middle of K (the fp32 sums of integers do
+  // not depend on the order), so the two blocks on a CU reach their
+  // epilogues half a tile apart and one runs its MFMAs while the other
+  // stores.
+  const int koff =
+      (WAVES == 4 && static_cast<int>(blockIdx.x / kNumXcd) >= grid_blocks / kNumXcd / 2) ? T / 2 : 0;
+  auto rot = [&](int st) __attribute__((always_inline)) { return st + koff < T ? st + koff : st + koff - T; };
 
   // Stage `st` of the tile at (m0, n0): activations into slot k, weights into w.
   auto issue_dma = [&](int m0, int st, int k) __attribute__((always_inline)) {
@@ -375,14 +405,15 @@ __global__ __launch_bounds__(kF6Threads, 1) void w4a4_f6_gemm_kernel(
 #pragma unroll
     for (int j = 0; j < kDmaPerWave; ++j) {
       const uint32_t band = static_cast<uint32_t>(min(m0 / 32 + rband[j], mbands - 1));
-      dma16(rsx, dst + 64 * j, rpart[j] == kOutside ? kOutside : band * band_bytes + rpart[j], 2 * kFragBytes * st);
+      dma16(rsx, dst + 64 * j, rpart[j] == kOutside ? kOutside : band * band_bytes + rpart[j],
+            2 * kFragBytes * rot(st));
     }
   };
   auto load_w = [&](WFrag& w, int n0, int st) __attribute__((always_inline)) {
 #pragma unroll
     for (int f = 0; f < 2; ++f) {
       const uint32_t wb = static_cast<uint32_t>(min(n0 / 32 + 2 * wn + f, nbands - 1)) * band_bytes;
-      const int so = 2 * st * kFragBytes;
+      const int so = 2 * rot(st) * kFragBytes;
       const v4i32 p0 = __builtin_bit_cast(v4i32, __builtin_amdgcn_raw_buffer_load_b128(rsw, wb + 16 * lane, so, 0));
       const v4i32 p1 =
           __builtin_bit_cast(v4i32, __builtin_amdgcn_raw_buffer_load_b128(rsw, wb + 1024 + 16 * lane, so, 0));
@@ -396,7 +427,24 @@ __global__ __launch_bounds__(kF6Threads, 1) void w4a4_f6_gemm_kernel(
   // quarter of s_x each, waves 4..7 a quarter of s_w, waves 0..1 half of the
   // bias.  Entries past M or N read as zero (outside the buffers).
   auto issue_scales = [&](int m0, int n0) __attribute__((always_inline)) {
-    if constexpr (EPI == Epilogue::kBf16) {
+    if constexpr (EPI == Epilogue::kBf16 && WAVES == 4) {
+      // every wave a quarter of s_w; waves 0, 1 half of s_x each, waves 2, 3
+      // half of the bias each
+      {
+        const __amdgpu_buffer_rsrc_t r =
+            __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(sw), 0, 4 * N, kBufferFlags);
+        dma4(r, sc_w + 64 * wave, 4 * static_cast<uint32_t>(n0 + 64 * wave + lane), 0);
+      }
+      if (wave < 2) {
+        const __amdgpu_buffer_rsrc_t r =
+            __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(sx), 0, 4 * M, kBufferFlags);
+        dma4(r, sc_x + 64 * wave, 4 * static_cast<uint32_t>(m0 + 64 * wave + lane), 0);
+      } else if (HAS_BIAS) {
+        const __amdgpu_buffer_rsrc_t r =
+            __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(bias), 0, 2 * N, kBufferFlags);
+        dma4(r, sc_b + 64 * (wave - 2), 2 * static_cast<uint32_t>(n0 + 128 * (wave - 2) + 2 * lane), 0);
+      }
+    } else if constexpr (EPI == Epilogue::kBf16) {
       const int q = wave & 3;
       if (wave < 4) {
         const __amdgpu_buffer_rsrc_t r =
@@ -417,7 +465,7 @@ __global__ __launch_bounds__(kF6Threads, 1) void w4a4_f6_gemm_kernel(
   // B fragment (k-step s, band 4 wm + fm) from slot k: the 16-byte part and
   // the 8-byte part.
   auto read_b = [&](int k, int s, int fm) __attribute__((always_inline)) {
-    const uint8_t* p = reinterpret_cast<const uint8_t*>(slot(k)) + (s * 8 + 4 * wm + fm) * kFragBytes;
+    const uint8_t* p = reinterpret_cast<const uint8_t*>(slot(k)) + (s * S::kBands + 4 * wm + fm) * kFragBytes;
     return join(*reinterpret_cast<const v4i32*>(p + 16 * lane),
                 *reinterpret_cast<const v2i32*>(p + 1024 + 8 * lane));
   };
@@ -721,6 +769,17 @@ int f6_tile_bands(int64_t M, int64_t N, int64_t slots) {
   return best;
 }
 
+// Block shape of the GEMM.  One 8-wave block per CU on 224- or 256-row tiles
+// re-reads the operands least, and wins when 256-row tiles cover M exactly
+// or K is long.  Otherwise two 4-wave blocks per CU on 128-row tiles win:
+// 224-row tiles save less than their missing band (the wave that holds three
+// bands waits on the one beside it that holds four), and with short K a
+// tile's epilogue is a large share of its time, which the other block's
+// MFMAs fill.  Measured over M 1024..9216, K 2048..12288, N 3072..12288.
+int f6_block_waves(int64_t M, int64_t N, int64_t K, int64_t slots) {
+  return K > kShortK || f6_tile_bands(M, N, slots) == 8 ? 8 : 4;
+}
+
 hipError_t launch_quantize_rows_f6(const uint16_t* x, int64_t M, int64_t K, uint8_t* out, float* scale,
                                    hipStream_t st) {
   const int64_t ksteps = f6_ksteps(K);
@@ -750,8 +809,8 @@ hipError_t launch_int4_to_f6(const uint8_t* q, int64_t rows, int64_t K, uint8_t*
 hipError_t launch_w4a4_f6_gemm(Epilogue epi, const uint8_t* xf6, const float* sx, int64_t M, int64_t K,
                                const uint8_t* wf6, const float* sw, int64_t N, const uint16_t* bias, void* out,
                                hipStream_t st) {
-  // One block per CU at most (a block fills a CU's registers); each walks
-  // its tiles in turn.
+  // Block slots: one 8-wave block or two 4-wave blocks per CU (a block's
+  // registers fill half or all of the CU); each block walks its tiles in turn.
   int dev = 0, cus = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return e;
@@ -759,22 +818,32 @@ hipError_t launch_w4a4_f6_gemm(Epilogue epi, const uint8_t* xf6, const float* sx
   if (e != hipSuccess) return e;
   const int ksteps = static_cast<int>(f6_ksteps(K));
   const int64_t slots = std::max<int64_t>(kNumXcd, cus / kNumXcd * kNumXcd);
-  const int tile_bands = f6_tile_bands(M, N, slots);
+  const int waves = f6_block_waves(M, N, K, slots);
+  const int tile_bands = waves == 4 ? 4 : f6_tile_bands(M, N, slots);
   const int tiles_m = static_cast<int>((M + 32 * tile_bands - 1) / (32 * tile_bands));
   const int tiles_n = static_cast<int>((N + kFBN - 1) / kFBN);
   const int64_t T = static_cast<int64_t>(tiles_m) * tiles_n;
   const int64_t per_xcd = (T + kNumXcd - 1) / kNumXcd;
-  const int blocks = static_cast<int>(ksteps / 2 < 3 ? per_xcd * kNumXcd : std::min<int64_t>(per_xcd * kNumXcd, slots));
+  const int64_t block_slots = (8 / waves) * slots;
+  const int blocks =
+      static_cast<int>(ksteps / 2 < 3 ? per_xcd * kNumXcd : std::min<int64_t>(per_xcd * kNumXcd, block_slots));
   const int mbands = static_cast<int>((M + 31) / 32);
   const int nbands = static_cast<int>((N + 31) / 32);
   const int Mi = static_cast<int>(M), Ni = static_cast<int>(N);
-#define JQ_F6(E, B, BT)                                                                                  \
-  hipLaunchKernelGGL((w4a4_f6_gemm_kernel<E, B, BT>), dim3(blocks), dim3(kF6Threads), 0, st, xf6, sx, Mi, mbands, \
+#define JQ_F6(W, E, B, BT)                                                                                   \
+  hipLaunchKernelGGL((w4a4_f6_gemm_kernel<W, E, B, BT>), dim3(blocks), dim3(64 * W), 0, st, xf6, sx, Mi, mbands, \
                      wf6, sw, Ni, nbands, ksteps, bias, out, tile_bands, tiles_m, tiles_n, blocks)
-  if (epi == Epilogue::kInt32) JQ_F6(Epilogue::kInt32, false, false);
-  else if (bias != nullptr && (N & 1)) JQ_F6(Epilogue::kBf16, true, true);
-  else if (bias != nullptr) JQ_F6(Epilogue::kBf16, true, false);
-  else JQ_F6(Epilogue::kBf16, false, false);
+#define JQ_F6_EPI(W)                                                      \
+  if (epi == Epilogue::kInt32) JQ_F6(W, Epilogue::kInt32, false, false);  \
+  else if (bias != nullptr && (N & 1)) JQ_F6(W, Epilogue::kBf16, true, true); \
+  else if (bias != nullptr) JQ_F6(W, Epilogue::kBf16, true, false);      \
+  else JQ_F6(W, Epilogue::kBf16, false, false);
+  if (waves == 4) {
+    JQ_F6_EPI(4)
+  } else {
+    JQ_F6_EPI(8)
+  }
+#undef JQ_F6_EPI
 #undef JQ_F6
   return hipGetLastError();
 }

@@ -49,6 +49,9 @@ hipError_t launch_w4a4g_gemm(Epilogue epi, const uint8_t* qx, const float* sx, i
 // activation layout and the weight layout respectively.
 int64_t f6_ksteps(int64_t K);
 int64_t f6_operand_bytes(int64_t rows, int64_t K);
+// GEMM block shape for an M x K by K x N product on `slots` CUs: 4 (two 4-wave
+// blocks per CU) or 8 (one 8-wave block) waves.
+int f6_block_waves(int64_t M, int64_t N, int64_t K, int64_t slots);
 // GEMM tile height in bands of 32 rows (7 or 8) for an M x N output on `slots` CUs.
 int f6_tile_bands(int64_t M, int64_t N, int64_t slots);
 
