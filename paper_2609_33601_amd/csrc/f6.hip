@@ -94,6 +94,7 @@ typedef float v16f __attribute__((ext_vector_type(16)));
 typedef unsigned v6u __attribute__((ext_vector_type(6)));
 typedef float v16f32 __attribute__((ext_vector_type(16)));
 typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
+typedef unsigned v4u32 __attribute__((ext_vector_type(4)));
 
 constexpr int kFragBytes = 1536;          // one 32-row x 64-code fragment
 constexpr int kFBN = 256;                 // block tile columns
@@ -192,11 +193,15 @@ __device__ __forceinline__ int64_t row_of_block(int64_t b) {
 }
 
 // Per-token quantiser writing the BF6 operand.  One block per row of the
-// padded operand; thread i handles groups i + T j (j < NJ) of 32 codes, each
-// read with four 16-byte loads, and keeps them in registers between the
-// absmax and the quantisation.  The scale and the codes are those of
-// quantize_rows_kernel.  Padding rows (M <= row < 32 * ceil(M/32)) get zero
-// codes and no scale.
+// padded operand; thread i handles groups i + T j (j < NJ) of 32 codes and
+// keeps them in registers between the absmax and the quantisation.  A wave
+// reads its 64 groups (4 KiB) as four 1 KiB loads of whole cache lines and
+// hands each lane its own 64 bytes through LDS (the 16-byte chunk q of the
+// wave's 256 at slot q ^ ((q >> 4) & 15), so that neither the writes nor the
+// reads conflict).  The loads are non-temporal: the input is read once, and
+// left to the caches it would evict the operands of the GEMM that follows.
+// The scale and the codes are those of quantize_rows_kernel.  Padding rows
+// (M <= row < 32 * ceil(M/32)) get zero codes and no scale.
 template <int NJ>
 __global__ __launch_bounds__(512) void quantize_rows_f6_kernel(const uint16_t* __restrict__ x, int64_t M, int64_t K,
                                                                int64_t rows_padded, int64_t ksteps,
@@ -210,18 +215,42 @@ __global__ __launch_bounds__(512) void quantize_rows_f6_kernel(const uint16_t* _
   const int groups = static_cast<int>(2 * ksteps);
   const uint16_t* xr = x + (live ? row : 0) * K;
 
+  extern __shared__ v4u32 xt[];  // 256 chunks of 16 bytes per wave
+  v4u32* xw = xt + 256 * wave;
+  auto swz = [](int q) { return q ^ ((q >> 4) & 15); };
   uint4 v[NJ][4];
   u16x2 am = {0, 0};
 #pragma unroll
   for (int j = 0; j < NJ; ++j) {
-    const int64_t k = 32 * static_cast<int64_t>(threadIdx.x + T * j);
+    const int64_t base = 32 * static_cast<int64_t>(T * j + 64 * wave);
+    v4u32 t[4];
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
-      v[j][c] = (live && k < K) ? *reinterpret_cast<const uint4*>(xr + k + 8 * c) : make_uint4(0, 0, 0, 0);
-      am = __builtin_elementwise_max(am, __builtin_bit_cast(u16x2, v[j][c].x & 0x7FFF7FFFu));
-      am = __builtin_elementwise_max(am, __builtin_bit_cast(u16x2, v[j][c].y & 0x7FFF7FFFu));
-      am = __builtin_elementwise_max(am, __builtin_bit_cast(u16x2, v[j][c].z & 0x7FFF7FFFu));
-      am = __builtin_elementwise_max(am, __builtin_bit_cast(u16x2, v[j][c].w & 0x7FFF7FFFu));
+      // Out-of-range chunks (K padding, padding rows) load the first chunk
+      // of x and are zeroed; no branch, so the four loads issue together.
+      const int64_t e = base + 512 * c + 8 * lane;
+      const bool ok = live && e < K;
+      t[c] = __builtin_nontemporal_load(reinterpret_cast<const v4u32*>(ok ? xr + e : x));
+      if (!ok) t[c] = v4u32{0, 0, 0, 0};
+      am = __builtin_elementwise_max(am, __builtin_bit_cast(u16x2, t[c].x & 0x7FFF7FFFu));
+      am = __builtin_elementwise_max(am, __builtin_bit_cast(u16x2, t[c].y & 0x7FFF7FFFu));
+      am = __builtin_elementwise_max(am, __builtin_bit_cast(u16x2, t[c].z & 0x7FFF7FFFu));
+      am = __builtin_elementwise_max(am, __builtin_bit_cast(u16x2, t[c].w & 0x7FFF7FFFu));
+    }
+    // Only this wave touches its chunks, and LDS runs a wave's accesses in
+    // order: the fences just keep the compiler from moving them.
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+#pragma unroll
+    for (int c = 0; c < 4; ++c) xw[swz(64 * c + lane)] = t[c];
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const v4u32 r = xw[swz(4 * lane + c)];
+      v[j][c] = make_uint4(r.x, r.y, r.z, r.w);
     }
   }
   uint32_t amax = am.x > am.y ? am.x : am.y;
@@ -290,7 +319,6 @@ __global__ __launch_bounds__(256) void int4_to_f6_kernel(const uint8_t* __restri
 // GEMM
 
 typedef int v4i32 __attribute__((ext_vector_type(4)));
-typedef unsigned v4u32 __attribute__((ext_vector_type(4)));
 typedef unsigned v2u32 __attribute__((ext_vector_type(2)));
 typedef int v2i32 __attribute__((ext_vector_type(2)));
 
@@ -738,7 +766,8 @@ hipError_t launch_qf6(const uint16_t* x, int64_t M, int64_t K, int64_t ksteps, u
   const int64_t rows_padded = (M + 31) / 32 * 32;
   const int64_t groups_of_8_bands = (rows_padded / 32 + kNumXcd - 1) / kNumXcd;
   const dim3 grid(static_cast<unsigned>(groups_of_8_bands * 32 * kNumXcd));
-  hipLaunchKernelGGL(quantize_rows_f6_kernel<NJ>, grid, dim3(threads), 0, st, x, M, K, rows_padded, ksteps, out, s);
+  const size_t lds = static_cast<size_t>(threads / 64) * 256 * 16;
+  hipLaunchKernelGGL(quantize_rows_f6_kernel<NJ>, grid, dim3(threads), lds, st, x, M, K, rows_padded, ksteps, out, s);
   return hipGetLastError();
 }
 
