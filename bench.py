@@ -23,9 +23,9 @@ launches on, and the CPU oracle timed on the whole step on the host cores
 with the GPU's.
 
 `secondary` reports, from the same run, the same measurement for other
-layers: the FLUX MLP step with ternary weights (W1.58A4) and group-wise
-(group64), the 8B diffusion-LLM block linears (W4A4 on both engines, W1.58A4,
-group128) and the DiT attention projection and fused QKV linears.
+layers: the FLUX MLP step with ternary weights (W1.58A4, on both engines) and
+group-wise (group64), the 8B diffusion-LLM block linears (W4A4 and W1.58A4 on
+both engines, group128) and the DiT attention projection and fused QKV linears.
 """
 
 import argparse
@@ -96,7 +96,8 @@ class Prepared:
     """Device-resident inputs, packed weight and output/workspace buffers of one linear.
 
     fmt "int4" packs the weight for the W4A4 layer (int8 engine), "bf6" for
-    the same layer on the bf6 engine, "ternary" for W1.58A4, "group64" /
+    the same layer on the bf6 engine, "ternary" for W1.58A4 (int8 engine),
+    "ternary_bf6" for W1.58A4 on the bf6 engine, "group64" /
     "group128" for group-wise W4A4 with that group size.
     """
 
@@ -120,6 +121,12 @@ class Prepared:
             self.wq = jq.jq_int4_to_f6_weight(self.wq4)
             self.linear = jq.jq_w4a4_f6_linear
             ws_bytes = jq.jq_w4a4_f6_workspace_bytes(lin.M, lin.K)
+        elif fmt == "ternary_bf6":
+            wt, self.sw = jq.jq_pack_weight_ternary(w)
+            self.wq = jq.jq_ternary_to_f6_weight(wt)
+            del wt
+            self.linear = jq.jq_w4a4_f6_linear
+            ws_bytes = jq.jq_w4a4_f6_workspace_bytes(lin.M, lin.K)
         else:
             pack = jq.jq_pack_weight_ternary if fmt == "ternary" else jq.jq_pack_weight_int4
             self.linear = jq.jq_w158a4_linear if fmt == "ternary" else jq.jq_w4a4_linear
@@ -130,7 +137,7 @@ class Prepared:
         self.ws = torch.empty(ws_bytes, dtype=torch.uint8, device="cuda")
         self.q = torch.empty((lin.M, lin.K // 2), dtype=torch.uint8, device="cuda")
         self.s = torch.empty((lin.M,), dtype=torch.float32, device="cuda")
-        if fmt == "bf6":
+        if fmt in ("bf6", "ternary_bf6"):
             self.q = torch.empty((jq.jq_f6_operand_bytes(lin.M, lin.K),), dtype=torch.uint8, device="cuda")
 
 
@@ -198,8 +205,9 @@ def time_step(torch, preps, steps, warmup):
 
 
 def secondary(torch, jq, workloads, steps):
-    cases = [(workloads.FLUX_MLP, "ternary"), (workloads.WORKLOADS["dllm_block"], "bf6"),
-             (workloads.WORKLOADS["dllm_block"], "int4"), (workloads.WORKLOADS["dllm_block"], "ternary"),
+    cases = [(workloads.FLUX_MLP, "ternary_bf6"), (workloads.FLUX_MLP, "ternary"),
+             (workloads.WORKLOADS["dllm_block"], "bf6"), (workloads.WORKLOADS["dllm_block"], "int4"),
+             (workloads.WORKLOADS["dllm_block"], "ternary_bf6"), (workloads.WORKLOADS["dllm_block"], "ternary"),
              (workloads.WORKLOADS["attn_proj"], "bf6"), (workloads.WORKLOADS["attn_proj"], "int4"),
              (workloads.WORKLOADS["qkv"], "bf6"), (workloads.WORKLOADS["qkv"], "int4"),
              (workloads.FLUX_MLP, "group64"), (workloads.WORKLOADS["dllm_block"], "group128")]
@@ -208,7 +216,8 @@ def secondary(torch, jq, workloads, steps):
         preps = [Prepared(lin, torch, jq, fmt) for lin in wl.linears]
         us = time_step(torch, preps, steps, warmup=5)
         tops = wl.ops / (us * 1e-6) / 1e12
-        layer = {"ternary": "W1.58A4", "int4": "W4A4 (int8 engine)", "bf6": "W4A4 (bf6 engine)"}.get(
+        layer = {"ternary": "W1.58A4 (int8 engine)", "ternary_bf6": "W1.58A4 (bf6 engine)",
+                 "int4": "W4A4 (int8 engine)", "bf6": "W4A4 (bf6 engine)"}.get(
             fmt, f"W4A4 {fmt}")
         log(f"secondary {wl.name} {layer}: {us:.1f} us/step, {tops:.0f} effective TOPS")
         out.append({"workload": wl.description, "layer": layer, "us_per_step": us, "effective_TOPS": tops,

@@ -372,6 +372,19 @@ jq_status jq_int4_to_f6(const void* q_packed, int64_t rows, int64_t K, void* f6,
 jq_status jq_int4_to_f6_weight(const void* q_packed, int64_t rows, int64_t K, void* wf6, void* stream);
 
 /*
+ * W1.58A4 on the BF6 engine.  Ternary codes -1, 0, 1 are int4 codes, so the
+ * W1.58A4 layer (acc = sum_k qx[m,k] * t[n,k], epilogue with g[n] in place of
+ * the int4 weight scale) is jq_w4a4_f6_linear / jq_w4a4_f6_gemm given the
+ * ternary codes in the BF6 weight layout and g as w_scale; the result is
+ * bit-identical to jq_w158a4_linear / jq_w158a4_gemm.  This re-encodes the
+ * packed ternary codes once per layer at model load, losslessly.
+ *   wt_packed in   [rows,K/4] uint8 from jq_pack_weight_ternary, 16-byte aligned
+ *   wf6       out  jq_f6_operand_bytes(rows,K) bytes, 16-byte aligned
+ * Errors: as jq_int4_to_f6.
+ */
+jq_status jq_ternary_to_f6_weight(const void* wt_packed, int64_t rows, int64_t K, void* wf6, void* stream);
+
+/*
  * Bytes of device workspace jq_w4a4_f6_linear needs for an [M,K] input: the
  * BF6 activation operand and the scales (4*M bytes), each part rounded up to
  * 256 bytes.  0 for invalid sizes.

@@ -290,10 +290,11 @@ __global__ __launch_bounds__(512) void quantize_rows_f6_kernel(const uint16_t* _
   }
 }
 
-// Canonical packed int4 codes -> BF6 operand in the activation or the weight
-// layout.  One thread per (row, 32-code group) of the padded operand; padding
-// rows and codes are written as zeros.
-template <bool WLAYOUT>
+// Canonical packed int4 codes (TERNARY false) or packed ternary codes (true)
+// -> BF6 operand in the activation or the weight layout.  One thread per
+// (row, 32-code group) of the padded operand; padding rows and codes are
+// written as zeros.
+template <bool WLAYOUT, bool TERNARY>
 __global__ __launch_bounds__(256) void int4_to_f6_kernel(const uint8_t* __restrict__ q, int64_t rows,
                                                          int64_t rows_padded, int64_t K, int64_t ksteps,
                                                          uint8_t* __restrict__ out) {
@@ -302,16 +303,27 @@ __global__ __launch_bounds__(256) void int4_to_f6_kernel(const uint8_t* __restri
   if (i >= rows_padded * groups) return;
   const int64_t row = i / groups;
   const int gi = static_cast<int>(i % groups);
-  uint4 p = make_uint4(0, 0, 0, 0);
-  if (row < rows && 32 * static_cast<int64_t>(gi) < K)
-    p = *reinterpret_cast<const uint4*>(q + row * (K / 2) + 16 * static_cast<int64_t>(gi));
-  const uint32_t w[4] = {p.x, p.y, p.z, p.w};
+  const bool live = row < rows && 32 * static_cast<int64_t>(gi) < K;
   float c[32];
+  if constexpr (!TERNARY) {
+    uint4 p = make_uint4(0, 0, 0, 0);
+    if (live) p = *reinterpret_cast<const uint4*>(q + row * (K / 2) + 16 * static_cast<int64_t>(gi));
+    const uint32_t w[4] = {p.x, p.y, p.z, p.w};
 #pragma unroll
-  for (int d = 0; d < 4; ++d)
+    for (int d = 0; d < 4; ++d)
 #pragma unroll
-    for (int n = 0; n < 8; ++n)  // nibble n of dword d is code 8d + n (even codes in low nibbles)
-      c[8 * d + n] = static_cast<float>(static_cast<int>(w[d] << (28 - 4 * n)) >> 28);
+      for (int n = 0; n < 8; ++n)  // nibble n of dword d is code 8d + n (even codes in low nibbles)
+        c[8 * d + n] = static_cast<float>(static_cast<int>(w[d] << (28 - 4 * n)) >> 28);
+  } else {
+    uint2 p = make_uint2(0, 0);
+    if (live) p = *reinterpret_cast<const uint2*>(q + row * (K / 4) + 8 * static_cast<int64_t>(gi));
+    const uint32_t w[2] = {p.x, p.y};
+#pragma unroll
+    for (int d = 0; d < 2; ++d)
+#pragma unroll
+      for (int n = 0; n < 16; ++n)  // 2-bit field n of dword d is code 16d + n
+        c[16 * d + n] = static_cast<float>(static_cast<int>(w[d] << (30 - 2 * n)) >> 30);
+  }
   store_group<WLAYOUT>(out, ksteps, row, gi, bf6_group(c));
 }
 
@@ -823,15 +835,20 @@ hipError_t launch_quantize_rows_f6(const uint16_t* x, int64_t M, int64_t K, uint
 }
 
 hipError_t launch_int4_to_f6(const uint8_t* q, int64_t rows, int64_t K, uint8_t* out, bool weight_layout,
-                             hipStream_t st) {
+                             bool ternary, hipStream_t st) {
   const int64_t ksteps = f6_ksteps(K);
   const int64_t rows_padded = (rows + 31) / 32 * 32;
   const int64_t total = rows_padded * 2 * ksteps;
   const dim3 grid(static_cast<unsigned>((total + 255) / 256));
-  if (weight_layout)
-    hipLaunchKernelGGL(int4_to_f6_kernel<true>, grid, dim3(256), 0, st, q, rows, rows_padded, K, ksteps, out);
-  else
-    hipLaunchKernelGGL(int4_to_f6_kernel<false>, grid, dim3(256), 0, st, q, rows, rows_padded, K, ksteps, out);
+#define JQ_CVT(W, T) hipLaunchKernelGGL((int4_to_f6_kernel<W, T>), grid, dim3(256), 0, st, q, rows, rows_padded, K, ksteps, out)
+  if (ternary) {
+    if (weight_layout) JQ_CVT(true, true);
+    else JQ_CVT(false, true);
+  } else {
+    if (weight_layout) JQ_CVT(true, false);
+    else JQ_CVT(false, false);
+  }
+#undef JQ_CVT
   return hipGetLastError();
 }
 

@@ -343,7 +343,7 @@ jq_status jq_int4_to_f6(const void* q_packed, int64_t rows, int64_t K, void* f6,
   if (st != JQ_OK) return st;
   if (!aligned(q_packed, 16) || !aligned(f6, 16)) return JQ_ERR_MISALIGNED;
   return from_hip(jq::launch_int4_to_f6(static_cast<const uint8_t*>(q_packed), rows, K, static_cast<uint8_t*>(f6),
-                                        false, as_stream(stream)));
+                                        false, false, as_stream(stream)));
 }
 
 jq_status jq_int4_to_f6_weight(const void* q_packed, int64_t rows, int64_t K, void* wf6, void* stream) {
@@ -352,7 +352,16 @@ jq_status jq_int4_to_f6_weight(const void* q_packed, int64_t rows, int64_t K, vo
   if (st != JQ_OK) return st;
   if (!aligned(q_packed, 16) || !aligned(wf6, 16)) return JQ_ERR_MISALIGNED;
   return from_hip(jq::launch_int4_to_f6(static_cast<const uint8_t*>(q_packed), rows, K, static_cast<uint8_t*>(wf6),
-                                        true, as_stream(stream)));
+                                        true, false, as_stream(stream)));
+}
+
+jq_status jq_ternary_to_f6_weight(const void* wt_packed, int64_t rows, int64_t K, void* wf6, void* stream) {
+  if (wt_packed == nullptr || wf6 == nullptr) return JQ_ERR_INVALID_ARG;
+  const jq_status st = check_shape(rows, K);
+  if (st != JQ_OK) return st;
+  if (!aligned(wt_packed, 16) || !aligned(wf6, 16)) return JQ_ERR_MISALIGNED;
+  return from_hip(jq::launch_int4_to_f6(static_cast<const uint8_t*>(wt_packed), rows, K, static_cast<uint8_t*>(wf6),
+                                        true, true, as_stream(stream)));
 }
 
 size_t jq_w4a4_f6_workspace_bytes(int64_t M, int64_t K) { return f6_workspace_bytes(M, K); }

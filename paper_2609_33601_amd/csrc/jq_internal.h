@@ -59,10 +59,11 @@ int f6_tile_bands(int64_t M, int64_t N, int64_t slots);
 hipError_t launch_quantize_rows_f6(const uint16_t* x, int64_t M, int64_t K, uint8_t* out, float* scale,
                                    hipStream_t st);
 
-// Canonical packed int4 codes -> BF6 operand in the activation layout or the
+// Canonical packed int4 codes ([rows, K/2]) or packed ternary codes
+// ([rows, K/4], `ternary`) -> BF6 operand in the activation layout or the
 // weight layout (padding written as zeros).
 hipError_t launch_int4_to_f6(const uint8_t* q, int64_t rows, int64_t K, uint8_t* out, bool weight_layout,
-                             hipStream_t st);
+                             bool ternary, hipStream_t st);
 
 // GEMM on BF6 operands (xf6 in the activation layout, wf6 in the weight
 // layout); epi is kBf16 (y = bf16(((acc*sx)*sw)+bias)) or kInt32 (acc).

@@ -44,6 +44,7 @@ SIGNATURES = {
     "jq_quantize_act_f6": (ctypes.c_int, [_vp, _i64, _i64, _vp, _fp, _vp]),
     "jq_int4_to_f6": (ctypes.c_int, [_vp, _i64, _i64, _vp, _vp]),
     "jq_int4_to_f6_weight": (ctypes.c_int, [_vp, _i64, _i64, _vp, _vp]),
+    "jq_ternary_to_f6_weight": (ctypes.c_int, [_vp, _i64, _i64, _vp, _vp]),
     "jq_w4a4_f6_workspace_bytes": (_sz, [_i64, _i64]),
     "jq_w4a4_f6_linear": (ctypes.c_int, [_vp, _i64, _i64, _vp, _fp, _i64, _vp, _vp, _vp, _sz, _vp]),
     "jq_w4a4_f6_gemm": (ctypes.c_int, [_vp, _fp, _i64, _i64, _vp, _fp, _i64, _vp, _vp, _vp]),
@@ -390,13 +391,14 @@ def jq_quantize_act_f6(x, xf6=None, scale=None, stream=None):
     return xf6, scale
 
 
-def _int4_to_f6(name, q, out, stream):
+def _int4_to_f6(name, q, out, stream, codes_per_byte=2):
     torch = _torch()
-    rows, Kh = q.shape
-    nb = jq_f6_operand_bytes(rows, 2 * Kh)
+    rows, Kb = q.shape
+    K = codes_per_byte * Kb
+    nb = jq_f6_operand_bytes(rows, K)
     if out is None:
         out = torch.empty((nb,), dtype=torch.uint8, device=q.device)
-    st = getattr(lib(), name)(_dev(q, torch.uint8, (rows, Kh), "q"), rows, 2 * Kh,
+    st = getattr(lib(), name)(_dev(q, torch.uint8, (rows, Kb), "q"), rows, K,
                               _dev(out, torch.uint8, (nb,), "out"), _stream_ptr(stream))
     _check(st, name)
     return out
@@ -410,6 +412,13 @@ def jq_int4_to_f6(q, out=None, stream=None):
 def jq_int4_to_f6_weight(q, out=None, stream=None):
     """Packed int4 codes uint8 [rows,K/2] -> BF6 operand, weight layout, uint8 [jq_f6_operand_bytes(rows,K)]."""
     return _int4_to_f6("jq_int4_to_f6_weight", q, out, stream)
+
+
+def jq_ternary_to_f6_weight(wt, out=None, stream=None):
+    """Packed ternary codes uint8 [rows,K/4] -> BF6 operand, weight layout, uint8 [jq_f6_operand_bytes(rows,K)].
+
+    With the ternary scales as w_scale, jq_w4a4_f6_linear then computes the W1.58A4 layer."""
+    return _int4_to_f6("jq_ternary_to_f6_weight", wt, out, stream, codes_per_byte=4)
 
 
 def jq_w4a4_f6_linear(x, wf6, w_scale, bias=None, y=None, workspace=None, stream=None):

@@ -31,7 +31,7 @@ def header_functions():
 
 def test_exports_every_declared_symbol():
     names = header_functions()
-    assert len(names) == 26, names
+    assert len(names) == 27, names
     lib = ctypes.CDLL(jq.LIB_PATH)
     for n in names:
         assert hasattr(lib, n), f"libjq.so does not export {n}"
@@ -206,6 +206,12 @@ def test_f6_quantize_and_convert_validation():
     assert L.jq_int4_to_f6_weight(A, 0, 64, A, None) == jq.JQ_ERR_INVALID_ARG
     assert L.jq_int4_to_f6_weight(A, 8, 96, A, None) == jq.JQ_ERR_UNSUPPORTED_SHAPE
     assert L.jq_int4_to_f6_weight(MIS, 8, 64, A, None) == jq.JQ_ERR_MISALIGNED
+    assert L.jq_ternary_to_f6_weight(None, 8, 64, A, None) == jq.JQ_ERR_INVALID_ARG
+    assert L.jq_ternary_to_f6_weight(A, 8, 64, None, None) == jq.JQ_ERR_INVALID_ARG
+    assert L.jq_ternary_to_f6_weight(A, 0, 64, A, None) == jq.JQ_ERR_INVALID_ARG
+    assert L.jq_ternary_to_f6_weight(A, 8, 96, A, None) == jq.JQ_ERR_UNSUPPORTED_SHAPE
+    assert L.jq_ternary_to_f6_weight(MIS, 8, 64, A, None) == jq.JQ_ERR_MISALIGNED
+    assert L.jq_ternary_to_f6_weight(A, 8, 64, MIS, None) == jq.JQ_ERR_MISALIGNED
 
 
 def test_f6_gemm_and_linear_validation():

@@ -357,3 +357,75 @@ def test_f6_linear_full_size(lin):
     rows = _sample_rows(lin.M, seed=lin.N)
     ref = oracle.w4a4_linear_rows(x_bits, wq.cpu().numpy(), sw.cpu().numpy(), rows, b_bits)
     assert_bf16_close(jq.bf16_bits(y6[torch.from_numpy(rows).cuda()]), ref, lin.name)
+
+
+# ---------------------------------------------------------------------------
+# W1.58A4 on the BF6 engine: ternary codes in the BF6 weight layout
+# ---------------------------------------------------------------------------
+
+
+def rand_ternary(rows, K, seed):
+    return np.random.default_rng(seed).integers(-1, 2, size=(rows, K)).astype(np.int8)
+
+
+@pytest.mark.parametrize("rows,K", [(1, 64), (31, 128), (33, 192), (100, 4160), (64, 12288)])
+def test_ternary_to_f6_weight_lossless(rows, K):
+    t = rand_ternary(rows, K, seed=rows * 3 + K)
+    f6 = jq.jq_ternary_to_f6_weight(torch.from_numpy(oracle.pack_ternary(t)).cuda())
+    torch.cuda.synchronize()
+    ref = np.zeros((32 * ((rows + 31) // 32), 128 * ((K + 127) // 128)), np.int64)
+    ref[:rows, :K] = t
+    assert np.array_equal(decode_f6_weight(f6.cpu().numpy(), rows, K), ref)
+
+
+@pytest.mark.parametrize("M,N,K", [(3, 5, 128), (257, 255, 192), (2100, 9000, 448), (512, 768, 12288)])
+def test_f6_w158a4_gemm_i32_random_codes(M, N, K):
+    say("f6 ternary gemm i32", M, N, K)
+    qx = rand_packed(M, K, seed=M * 13 + K)
+    wt = oracle.pack_ternary(rand_ternary(N, K, seed=N * 17 + K))
+    xf6 = jq.jq_int4_to_f6(torch.from_numpy(qx).cuda())
+    wf6 = jq.jq_ternary_to_f6_weight(torch.from_numpy(wt).cuda())
+    acc = jq.jq_w4a4_f6_gemm_i32(xf6, M, K, wf6, N)
+    torch.cuda.synchronize()
+    ref = oracle.w158a4_gemm_i32(qx, wt)
+    bad = np.argwhere(acc.cpu().numpy() != ref)
+    assert bad.size == 0, f"{len(bad)} accumulators differ, first {bad[:4].tolist()}"
+
+
+def f6_ternary_layer(x_bits, w_bits, b_bits):
+    """The W1.58A4 layer on the BF6 engine and on the int8 engine, same inputs."""
+    x = dev_bf16(x_bits)
+    wt, g = jq.jq_pack_weight_ternary(dev_bf16(w_bits))
+    wf6 = jq.jq_ternary_to_f6_weight(wt)
+    b = None if b_bits is None else dev_bf16(b_bits)
+    y6 = jq.jq_w4a4_f6_linear(x, wf6, g, b)
+    y8 = jq.jq_w158a4_linear(x, wt, g, b)
+    torch.cuda.synchronize()
+    return y6, y8, wt.cpu().numpy(), g.cpu().numpy()
+
+
+@pytest.mark.parametrize("M,K,N,bias", [(77, 3072, 130, True), (1, 64, 1, False), (513, 256, 777, True),
+                                        (257, 4160, 300, True)])
+def test_f6_w158a4_linear_ragged(M, K, N, bias):
+    say("f6 ternary linear ragged", M, K, N, bias)
+    x = workloads.activations(M, K, "student_t3", M + 7, 0.01, 50.0)
+    w = workloads.weights(N, K, 0.02, N + 9)
+    b = workloads.bias(N, 0.01, 11) if bias else None
+    y6, y8, wt, g = f6_ternary_layer(x, w, b)
+    assert torch.equal(y6.view(torch.int16), y8.view(torch.int16))
+    assert_bf16_close(jq.bf16_bits(y6), oracle.w158a4_linear(x, wt, g, b), f"f6 ternary {M}x{K}->{N}")
+
+
+@pytest.mark.parametrize("lin", [workloads.FLUX_MLP.linears[0], workloads.FLUX_MLP.linears[1],
+                                 workloads.WORKLOADS["dllm_block"].linears[0]], ids=lambda l: l.name)
+def test_f6_w158a4_linear_full_size(lin):
+    """Full-size W1.58A4 layer on the BF6 engine: bit-identical to the int8
+    engine's W1.58A4 layer, sampled rows vs the oracle."""
+    say("f6 ternary linear full", lin.name, lin.M, lin.K, lin.N)
+    x_bits, w_bits, b_bits = lin.make_x(), lin.make_w(), lin.make_bias()
+    y6, y8, wt, g = f6_ternary_layer(x_bits, w_bits, b_bits)
+    diff = int((y6.view(torch.int16) != y8.view(torch.int16)).sum())
+    assert diff == 0, f"{diff} outputs differ from the int8 engine's W1.58A4 layer"
+    rows = _sample_rows(lin.M, seed=lin.N + 1)
+    ref = oracle.w158a4_linear_rows(x_bits, wt, g, rows, b_bits)
+    assert_bf16_close(jq.bf16_bits(y6[torch.from_numpy(rows).cuda()]), ref, lin.name)
