@@ -93,6 +93,8 @@ __device__ __forceinline__ uint32_t pack8_fast(uint4 v, float rcp, bool* near) {
   return (e & 0x0F0F0F0Fu) | ((o << 4) & 0xF0F0F0F0u);
 }
 
+typedef unsigned v4u32 __attribute__((ext_vector_type(4)));
+
 __device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) {
@@ -104,6 +106,9 @@ __device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
 
 // One block per row: W = blockDim.x / 64 waves share the row, wave w owning
 // chunks w*NC .. w*NC + NC - 1 (chunk c = elements [c*512, c*512 + 512)).
+// The input is read once, with non-temporal loads, so that it does not evict
+// the operands of the GEMM that follows; chunks past K load the first chunk
+// of x and are discarded.
 template <int NC>
 __global__ __launch_bounds__(512) void quantize_rows_kernel(
     const uint16_t* __restrict__ x, int64_t M, int64_t K,
@@ -122,10 +127,10 @@ __global__ __launch_bounds__(512) void quantize_rows_kernel(
 #pragma unroll
   for (int c = 0; c < NC; ++c) {
     const int64_t k = static_cast<int64_t>(wave * NC + c) * 512 + lane * 8;
-    if (k < K) {
-      v[c] = *reinterpret_cast<const uint4*>(xr + k);
-    } else {
-      v[c] = make_uint4(0, 0, 0, 0);
+    {
+      const bool ok = k < K;
+      const v4u32 t = __builtin_nontemporal_load(reinterpret_cast<const v4u32*>(ok ? xr + k : x));
+      v[c] = ok ? make_uint4(t.x, t.y, t.z, t.w) : make_uint4(0, 0, 0, 0);
     }
     am = __builtin_elementwise_max(am, __builtin_bit_cast(u16x2, v[c].x & 0x7FFF7FFFu));
     am = __builtin_elementwise_max(am, __builtin_bit_cast(u16x2, v[c].y & 0x7FFF7FFFu));
@@ -224,7 +229,7 @@ __global__ __launch_bounds__(256) void quantize_rows_stream_kernel(
 // no group straddles two rows, so the scale of unit i is scale[i / (G/8)]
 // in the row-major [rows, K/G] layout.  The quotient uses the same
 // reciprocal-with-exact-fallback path as the per-row kernel, with one
-// reciprocal per group.
+// reciprocal per group.  Non-temporal loads, as in the per-row kernel.
 template <int G>
 __global__ __launch_bounds__(256) void quantize_groups_kernel(const uint16_t* __restrict__ x, int64_t units,
                                                               uint8_t* __restrict__ q, float* __restrict__ scale) {
@@ -232,7 +237,10 @@ __global__ __launch_bounds__(256) void quantize_groups_kernel(const uint16_t* __
   const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
   const bool live = i < units;
   uint4 v = make_uint4(0, 0, 0, 0);
-  if (live) v = reinterpret_cast<const uint4*>(x)[i];
+  if (live) {
+    const v4u32 t = __builtin_nontemporal_load(reinterpret_cast<const v4u32*>(x) + i);
+    v = make_uint4(t.x, t.y, t.z, t.w);
+  }
   u16x2 am = __builtin_bit_cast(u16x2, v.x & 0x7FFF7FFFu);
   am = __builtin_elementwise_max(am, __builtin_bit_cast(u16x2, v.y & 0x7FFF7FFFu));
   am = __builtin_elementwise_max(am, __builtin_bit_cast(u16x2, v.z & 0x7FFF7FFFu));
