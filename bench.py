@@ -24,8 +24,9 @@ with the GPU's.
 
 `secondary` reports, from the same run, the same measurement for other
 layers: the FLUX MLP step with ternary weights (W1.58A4, on both engines) and
-group-wise (group64), the 8B diffusion-LLM block linears (W4A4 and W1.58A4 on
-both engines, group128) and the DiT attention projection and fused QKV linears.
+group-wise (group64, on both engines), the 8B diffusion-LLM block linears
+(W4A4, W1.58A4 and group128, each on both engines) and the DiT attention
+projection and fused QKV linears.
 """
 
 import argparse
@@ -98,7 +99,8 @@ class Prepared:
     fmt "int4" packs the weight for the W4A4 layer (int8 engine), "bf6" for
     the same layer on the bf6 engine, "ternary" for W1.58A4 (int8 engine),
     "ternary_bf6" for W1.58A4 on the bf6 engine, "group64" /
-    "group128" for group-wise W4A4 with that group size.
+    "group128" for group-wise W4A4 with that group size (int8 engine), and
+    "group64_bf6" / "group128_bf6" for the same on the bf6 engine.
     """
 
     def __init__(self, lin, torch, jq, fmt="int4"):
@@ -110,7 +112,15 @@ class Prepared:
         self.x = jq.bf16_tensor(self.x_bits, "cuda")
         w = jq.bf16_tensor(self.w_bits, "cuda")
         ws_bytes = jq.jq_w4a4_workspace_bytes(lin.M, lin.K)
-        if fmt.startswith("group"):
+        if fmt.startswith("group") and fmt.endswith("_bf6"):
+            G = int(fmt[5:-4])
+            wq4, self.sw = jq.jq_pack_weight_int4_group(w, G)
+            self.wq = jq.jq_int4_to_f6_weight(wq4)
+            del wq4
+            self.linear = lambda x, wq, sw, b, y, workspace: jq.jq_w4a4g_f6_linear(x, wq, sw, G, b, y=y,
+                                                                                  workspace=workspace)
+            ws_bytes = jq.jq_w4a4g_f6_workspace_bytes(lin.M, lin.K, G)
+        elif fmt.startswith("group"):
             G = int(fmt[5:])
             self.wq, self.sw = jq.jq_pack_weight_int4_group(w, G)
             self.linear = lambda x, wq, sw, b, y, workspace: jq.jq_w4a4g_linear(x, wq, sw, G, b, y=y,
@@ -210,15 +220,17 @@ def secondary(torch, jq, workloads, steps):
              (workloads.WORKLOADS["dllm_block"], "ternary_bf6"), (workloads.WORKLOADS["dllm_block"], "ternary"),
              (workloads.WORKLOADS["attn_proj"], "bf6"), (workloads.WORKLOADS["attn_proj"], "int4"),
              (workloads.WORKLOADS["qkv"], "bf6"), (workloads.WORKLOADS["qkv"], "int4"),
-             (workloads.FLUX_MLP, "group64"), (workloads.WORKLOADS["dllm_block"], "group128")]
+             (workloads.FLUX_MLP, "group64_bf6"), (workloads.FLUX_MLP, "group64"),
+             (workloads.WORKLOADS["dllm_block"], "group128_bf6"), (workloads.WORKLOADS["dllm_block"], "group128")]
     out = []
     for wl, fmt in cases:
         preps = [Prepared(lin, torch, jq, fmt) for lin in wl.linears]
         us = time_step(torch, preps, steps, warmup=5)
         tops = wl.ops / (us * 1e-6) / 1e12
         layer = {"ternary": "W1.58A4 (int8 engine)", "ternary_bf6": "W1.58A4 (bf6 engine)",
-                 "int4": "W4A4 (int8 engine)", "bf6": "W4A4 (bf6 engine)"}.get(
-            fmt, f"W4A4 {fmt}")
+                 "int4": "W4A4 (int8 engine)", "bf6": "W4A4 (bf6 engine)",
+                 "group64": "W4A4 group64 (int8 engine)", "group128": "W4A4 group128 (int8 engine)",
+                 "group64_bf6": "W4A4 group64 (bf6 engine)", "group128_bf6": "W4A4 group128 (bf6 engine)"}[fmt]
         log(f"secondary {wl.name} {layer}: {us:.1f} us/step, {tops:.0f} effective TOPS")
         out.append({"workload": wl.description, "layer": layer, "us_per_step": us, "effective_TOPS": tops,
                     "pct_int8_peak": 100.0 * tops / PEAK_INT8_TOPS,

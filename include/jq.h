@@ -426,6 +426,66 @@ jq_status jq_w4a4_f6_gemm(const void* xf6, const float* scale, int64_t M, int64_
 jq_status jq_w4a4_f6_gemm_i32(const void* xf6, int64_t M, int64_t K,
                               const void* wf6, int64_t N, int32_t* acc, void* stream);
 
+/*
+ * ---------------------------------------------------------------------------
+ * Group-wise W4A4 on the BF6 engine.
+ *
+ * The group-wise layer defined above (the same codes, scales [rows, K/G],
+ * the fp32 group sum in k order and the epilogue), with the codes held as
+ * BF6 operands: the matrix cores return each group's exact integer product
+ * in fp32, so the result is bit-identical to jq_w4a4g_linear.  Weights:
+ * jq_pack_weight_int4_group, then jq_int4_to_f6_weight on its codes; its
+ * scales are used as they are.  Shapes and errors as for the group-wise
+ * layer, plus the BF6 operand limits (each operand below 2 GiB).
+ */
+
+/*
+ * Group-wise activation quantisation into the BF6 activation layout.
+ *   x_bf16  in   [M,K] bf16, 16-byte aligned
+ *   xf6     out  jq_f6_operand_bytes(M,K) bytes, 16-byte aligned
+ *   scales  out  [M,K/G] fp32, 4-byte aligned
+ * Errors: JQ_ERR_INVALID_ARG, JQ_ERR_UNSUPPORTED_SHAPE, JQ_ERR_MISALIGNED, JQ_ERR_HIP.
+ */
+jq_status jq_quantize_act_group_f6(const void* x_bf16, int64_t M, int64_t K, int64_t G,
+                                   void* xf6, float* scales, void* stream);
+
+/*
+ * Bytes of device workspace jq_w4a4g_f6_linear needs: the BF6 activation
+ * operand and its scales (4*M*K/G bytes), each rounded up to 256 bytes.
+ * 0 for invalid sizes.
+ */
+size_t jq_w4a4g_f6_workspace_bytes(int64_t M, int64_t K, int64_t G);
+
+/*
+ * The whole group-wise W4A4 linear on the BF6 engine.
+ *   wf6        in   BF6 weight operand (weight layout) of the group-packed codes
+ *   w_scales   in   [N,K/G] fp32 from jq_pack_weight_int4_group
+ *   workspace  at least jq_w4a4g_f6_workspace_bytes(M,K,G) bytes, 256-byte aligned
+ *   other arguments as jq_w4a4g_linear
+ * Errors: as jq_w4a4g_linear.
+ */
+jq_status jq_w4a4g_f6_linear(const void* x_bf16, int64_t M, int64_t K, int64_t G,
+                             const void* wf6, const float* w_scales, int64_t N,
+                             const void* bias_bf16, void* y_bf16,
+                             void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Group GEMM + epilogue on a BF6 activation operand and its scales (from
+ * jq_quantize_act_group_f6); other arguments as jq_w4a4g_f6_linear.
+ * Errors: JQ_ERR_INVALID_ARG, JQ_ERR_UNSUPPORTED_SHAPE, JQ_ERR_MISALIGNED, JQ_ERR_HIP.
+ */
+jq_status jq_w4a4g_f6_gemm(const void* xf6, const float* scales, int64_t M, int64_t K, int64_t G,
+                           const void* wf6, const float* w_scales, int64_t N,
+                           const void* bias_bf16, void* y_bf16, void* stream);
+
+/*
+ * The fp32 group sum S[m,n] alone, for checking: the same kernel as
+ * jq_w4a4g_f6_gemm storing S into s_f32 [M,N] (16-byte aligned).
+ * Errors: as jq_w4a4g_f6_gemm.
+ */
+jq_status jq_w4a4g_f6_gemm_f32(const void* xf6, const float* scales, int64_t M, int64_t K, int64_t G,
+                               const void* wf6, const float* w_scales, int64_t N, float* s_f32, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -202,7 +202,11 @@ __device__ __forceinline__ int64_t row_of_block(int64_t b) {
 // left to the caches it would evict the operands of the GEMM that follows.
 // The scale and the codes are those of quantize_rows_kernel.  Padding rows
 // (M <= row < 32 * ceil(M/32)) get zero codes and no scale.
-template <int NJ>
+//
+// G = 64 or 128: one scale per G consecutive codes instead (scale [M, K/G]
+// row-major, the codes and scales of quantize_groups_kernel).  A group is the
+// 32-code groups of G/32 neighbouring lanes, which meet with shuffles.
+template <int NJ, int G>
 __global__ __launch_bounds__(512) void quantize_rows_f6_kernel(const uint16_t* __restrict__ x, int64_t M, int64_t K,
                                                                int64_t rows_padded, int64_t ksteps,
                                                                uint8_t* __restrict__ out, float* __restrict__ scale) {
@@ -252,6 +256,46 @@ __global__ __launch_bounds__(512) void quantize_rows_f6_kernel(const uint16_t* _
       const v4u32 r = xw[swz(4 * lane + c)];
       v[j][c] = make_uint4(r.x, r.y, r.z, r.w);
     }
+  }
+  if constexpr (G != 0) {
+    (void)am;
+    (void)wave_max;
+    constexpr int kLanes = G / 32;  // lanes per group
+    const int64_t KG = K / G;
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+      u16x2 gm = {0, 0};
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        gm = __builtin_elementwise_max(gm, __builtin_bit_cast(u16x2, v[j][c].x & 0x7FFF7FFFu));
+        gm = __builtin_elementwise_max(gm, __builtin_bit_cast(u16x2, v[j][c].y & 0x7FFF7FFFu));
+        gm = __builtin_elementwise_max(gm, __builtin_bit_cast(u16x2, v[j][c].z & 0x7FFF7FFFu));
+        gm = __builtin_elementwise_max(gm, __builtin_bit_cast(u16x2, v[j][c].w & 0x7FFF7FFFu));
+      }
+      uint32_t gmax = gm.x > gm.y ? gm.x : gm.y;
+#pragma unroll
+      for (int off = 1; off < kLanes; off <<= 1) {
+        const uint32_t o = static_cast<uint32_t>(__shfl_xor(static_cast<int>(gmax), off, 64));
+        gmax = gmax > o ? gmax : o;
+      }
+      const int gi = threadIdx.x + T * j;
+      if (gi >= groups) continue;
+      const float sg = __uint_as_float(gmax << 16) / 7.0f;
+      if (live && gi % kLanes == 0 && 32 * static_cast<int64_t>(gi) < K) scale[row * KG + gi / kLanes] = sg;
+      const float rcp = (sg == 0.0f) ? 0.0f : 1.0f / sg;
+      float q[32];
+      if (sg == 0.0f) {
+#pragma unroll
+        for (int p = 0; p < 32; ++p) q[p] = 0.0f;
+      } else {
+        const uint32_t w[16] = {v[j][0].x, v[j][0].y, v[j][0].z, v[j][0].w, v[j][1].x, v[j][1].y,
+                                v[j][1].z, v[j][1].w, v[j][2].x, v[j][2].y, v[j][2].z, v[j][2].w,
+                                v[j][3].x, v[j][3].y, v[j][3].z, v[j][3].w};
+        codes32(w, sg, rcp, __builtin_isinf(rcp), q);
+      }
+      store_group<false>(out, ksteps, row, gi, bf6_group(q));
+    }
+    return;
   }
   uint32_t amax = am.x > am.y ? am.x : am.y;
 #pragma unroll
@@ -772,14 +816,272 @@ __global__ __launch_bounds__(64 * WAVES, 8 / WAVES) void w4a4_f6_gemm_kernel(
   else run(std::integral_constant<int, 3>{});
 }
 
-template <int NJ>
+// ---------------------------------------------------------------------------
+// Group-wise GEMM on BF6 operands
+//
+// S[m,n] = sum over the groups g in k order of fl32(fl32(acc_g * s_x[m,g]) *
+// s_w[n,g]), acc_g the exact integer product over the G codes of group g (a
+// single k-step for G = 64, two for G = 128), then y = bf16(S + bias) (or S
+// itself, EPI kF32).  The matrix cores deliver acc_g in fp32, exactly, so the
+// fold after each group is two multiplies and an add per output: the kernel
+// is bound by that vector arithmetic, not by the MFMAs.
+//
+// Block tile 128 (m) x 128 (n), four waves, two blocks per CU; wave (wm, wn)
+// owns activation bands 2wm, 2wm + 1 and weight bands 2wn, 2wn + 1 of the
+// tile: 2 x 2 tiles of 32x32, 64 fp32 sums per lane.  A stage is 128 codes of
+// K: both operands' fragments (activation layout and weight layout, 12 KiB
+// each) move into LDS by buffer_load ... lds, one stage ahead, into two
+// slots; the stage's scales (s_x and s_w of its groups, gathered from the
+// [rows, K/G] arrays) follow through registers.  Operand bands past M or N
+// read as zero (outside the buffers).
+template <int G, Epilogue EPI, bool HAS_BIAS>
+__global__ __launch_bounds__(256, 2) void w4a4g_f6_gemm_kernel(
+    const uint8_t* __restrict__ xf6, const float* __restrict__ sx, int M, int mbands,
+    const uint8_t* __restrict__ wf6, const float* __restrict__ sw, int N, int nbands, int ksteps, int KG,
+    const uint16_t* __restrict__ bias, void* __restrict__ out, int tiles_m, int tiles_n) {
+  constexpr int kGps = 128 / G;                    // groups per stage
+  constexpr int kOpU4 = 4 * 2 * kFragBytes / 16;   // one operand's stage: 4 bands x 3072 bytes
+  // Two slots: the operand fragments of a stage (activations, then weights)
+  // and its scales (s_x, then s_w).  Accesses name the slot array directly,
+  // with the slot known at compile time, so that the compiler can tell the
+  // slot being read from the one the DMA is filling.
+  __shared__ uint4 op0[2 * kOpU4];
+  __shared__ uint4 op1[2 * kOpU4];
+  __shared__ float sc0[2 * kGps * 128];
+  __shared__ float sc1[2 * kGps * 128];
+  auto opk = [&](int k) __attribute__((always_inline)) { return k == 0 ? op0 : op1; };
+  auto sck = [&](int k) __attribute__((always_inline)) { return k == 0 ? sc0 : sc1; };
+
+  TileCoord tc;
+  if (!tile_of_block(blockIdx.x, tiles_m, tiles_n, &tc)) return;
+  const int m0 = 128 * tc.tm, n0 = 128 * tc.tn;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave >> 1, wn = wave & 1;
+  const int T = ksteps / 2;
+  const uint32_t band_bytes = static_cast<uint32_t>(ksteps) * kFragBytes;
+
+  const __amdgpu_buffer_rsrc_t rsx = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint8_t*>(xf6), 0, static_cast<int>(static_cast<int64_t>(mbands) * band_bytes), kBufferFlags);
+  const __amdgpu_buffer_rsrc_t rsw = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint8_t*>(wf6), 0, static_cast<int>(static_cast<int64_t>(nbands) * band_bytes), kBufferFlags);
+
+  // Operand DMA: the 12 KiB of a stage are 12 instructions of 1 KiB, three
+  // per wave; instruction i = 3 wave + j is part i % 3 of band i / 3.  Bands
+  // past the operand read as zero.
+  uint32_t xoff[3], woff[3];
+#pragma unroll
+  for (int j = 0; j < 3; ++j) {
+    const int i = 3 * wave + j;
+    const int b = i / 3, part = i % 3;
+    const int xb = m0 / 32 + b, wb = n0 / 32 + b;
+    xoff[j] = xb < mbands ? static_cast<uint32_t>(xb) * band_bytes + 1024 * part + 16 * lane : kOutside;
+    woff[j] = wb < nbands ? static_cast<uint32_t>(wb) * band_bytes + 1024 * part + 16 * lane : kOutside;
+  }
+  auto issue = [&](int u, int k) __attribute__((always_inline)) {
+    uint4* const xa = opk(k);
+    uint4* const wa = opk(k) + kOpU4;
+    const int so = 2 * kFragBytes * u;
+#pragma unroll
+    for (int j = 0; j < 3; ++j) {
+      dma16(rsx, xa + 64 * (3 * wave + j), xoff[j], so);  // kOutside + so stays outside
+      dma16(rsw, wa + 64 * (3 * wave + j), woff[j], so);
+    }
+  };
+  // The stage's scales, kGps * 128 of s_x and of s_w (entry e: group e / 128
+  // of row, or column, e % 128 of the tile; zero past M, N or K), go through
+  // registers: loaded with the stage's DMA, written to the scale slot once
+  // they have landed.  (Moved by DMA as well, some of their reads lost the
+  // alias information that tells the slots apart, and every such read
+  // waited for the next stage's DMA.)
+  float scv[2];
+  auto load_scales = [&](int u) __attribute__((always_inline)) {
+    if constexpr (kGps == 2) {
+      const int gl = tid >> 7, r = tid & 127, g = 2 * u + gl;
+      scv[0] = (m0 + r < M && g < KG) ? sx[static_cast<int64_t>(m0 + r) * KG + g] : 0.0f;
+      scv[1] = (n0 + r < N && g < KG) ? sw[static_cast<int64_t>(n0 + r) * KG + g] : 0.0f;
+    } else {
+      const int r = tid & 127;
+      if (tid < 128) scv[0] = m0 + r < M ? sx[static_cast<int64_t>(m0 + r) * KG + u] : 0.0f;
+      else scv[0] = n0 + r < N ? sw[static_cast<int64_t>(n0 + r) * KG + u] : 0.0f;
+    }
+  };
+  auto store_scales = [&](int k) __attribute__((always_inline)) {
+    sck(k)[tid] = scv[0];
+    if constexpr (kGps == 2) sck(k)[256 + tid] = scv[1];
+  };
+
+  v16f S[2][2];  // [weight band f][activation band fb]
+#pragma unroll
+  for (int f = 0; f < 2; ++f)
+#pragma unroll
+    for (int fb = 0; fb < 2; ++fb) S[f][fb] = v16f{};
+
+  // Fold one group into the sums: lane holds column m = 32 (2wm + fb) +
+  // (lane & 31) and rows n = 32 (2wn + f) + 8 j + 4 (lane >> 5) + r of y^T.
+  // The lane's scales of a stage, read from the scale slot before the next
+  // stage's DMA is issued (some of these reads lose the alias information
+  // that tells the slots apart and would otherwise wait for that DMA).
+  float xsr[kGps][2];
+  float4 wsr[kGps][2][4];
+  auto read_scales = [&](int k) __attribute__((always_inline)) {
+#pragma unroll
+    for (int gl = 0; gl < kGps; ++gl)
+#pragma unroll
+      for (int b = 0; b < 2; ++b) {
+        xsr[gl][b] = sck(k)[128 * gl + 32 * (2 * wm + b) + (lane & 31)];
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          wsr[gl][b][j] = *reinterpret_cast<const float4*>(sck(k) + kGps * 128 + 128 * gl + 32 * (2 * wn + b) +
+                                                           8 * j + 4 * (lane >> 5));
+      }
+  };
+  auto fold = [&](const v16f& acc, int f, int fb, int gl) __attribute__((always_inline)) {
+    const float xs = xsr[gl][fb];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const float wsa[4] = {wsr[gl][f][j].x, wsr[gl][f][j].y, wsr[gl][f][j].z, wsr[gl][f][j].w};
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        float t = acc[4 * j + r] * xs;
+        t = t * wsa[r];
+        S[f][fb][4 * j + r] = S[f][fb][4 * j + r] + t;
+      }
+    }
+  };
+  auto read_x = [&](int k, int t, int fb) __attribute__((always_inline)) {
+    const uint8_t* p = reinterpret_cast<const uint8_t*>(opk(k)) + (2 * wm + fb) * 2 * kFragBytes + t * kFragBytes;
+    return join(*reinterpret_cast<const v4i32*>(p + 16 * lane), *reinterpret_cast<const v2i32*>(p + 1024 + 8 * lane));
+  };
+  auto read_w = [&](int k, int t, int f) __attribute__((always_inline)) {
+    const uint8_t* p = reinterpret_cast<const uint8_t*>(opk(k) + kOpU4) + (2 * wn + f) * 2 * kFragBytes;
+    if (t == 0) {
+      const v4i32 a = *reinterpret_cast<const v4i32*>(p + 16 * lane);
+      const v2i32 b = *reinterpret_cast<const v2i32*>(p + 1024 + 16 * lane);
+      return v8i{a.x, a.y, a.z, a.w, b.x, b.y, 0, 0};
+    }
+    const v2i32 a = *reinterpret_cast<const v2i32*>(p + 1024 + 16 * lane + 8);
+    const v4i32 b = *reinterpret_cast<const v4i32*>(p + 2048 + 16 * lane);
+    return v8i{a.x, a.y, b.x, b.y, b.z, b.w, 0, 0};
+  };
+
+  // Stage u from slot (xa, wa, sxa, swa): the stage's loads have landed
+  // and every wave has passed the barrier after them.
+  auto compute = [&](int u, int k) __attribute__((always_inline)) {
+    if constexpr (G == 64) {
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        if (kGps * u + t >= KG) break;  // K % 128 == 64: the last stage's second half is padding
+        const v8i b0 = read_x(k, t, 0), b1 = read_x(k, t, 1);
+#pragma unroll
+        for (int f = 0; f < 2; ++f) {
+          const v8i a = read_w(k, t, f);
+          const v16f c0 = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b0, v16f{}, 3, 3, 0, 127, 0, 127);
+          const v16f c1 = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b1, v16f{}, 3, 3, 0, 127, 0, 127);
+          fold(c0, f, 0, t);
+          fold(c1, f, 1, t);
+        }
+      }
+    } else {
+      const v8i b00 = read_x(k, 0, 0), b01 = read_x(k, 0, 1);
+      const v8i b10 = read_x(k, 1, 0), b11 = read_x(k, 1, 1);
+#pragma unroll
+      for (int f = 0; f < 2; ++f) {
+        const v8i a0 = read_w(k, 0, f), a1 = read_w(k, 1, f);
+        v16f c0 = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a0, b00, v16f{}, 3, 3, 0, 127, 0, 127);
+        v16f c1 = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a0, b01, v16f{}, 3, 3, 0, 127, 0, 127);
+        c0 = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a1, b10, c0, 3, 3, 0, 127, 0, 127);
+        c1 = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a1, b11, c1, 3, 3, 0, 127, 0, 127);
+        fold(c0, f, 0, 0);
+        fold(c1, f, 1, 0);
+      }
+    }
+  };
+
+  // Two stages per iteration, one per slot: wait for the stage's loads,
+  // write its scales, meet at a barrier (every wave is then also done with
+  // the other slot), issue the next stage into the other slot, compute.
+  load_scales(0);
+  issue(0, 0);
+  for (int u = 0; u < T; u += 2) {
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+    store_scales(0);
+    __syncthreads();
+    read_scales(0);
+    if (u + 1 < T) {
+      load_scales(u + 1);  // before the DMA: a wait for them then counts past it
+      issue(u + 1, 1);
+    }
+    compute(u, 0);
+    if (u + 1 >= T) break;
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+    store_scales(1);
+    __syncthreads();
+    read_scales(1);
+    if (u + 2 < T) {
+      load_scales(u + 2);
+      issue(u + 2, 0);
+    }
+    compute(u + 1, 1);
+  }
+
+  // Epilogue: bias (bf16) added in fp32, rounded to bf16; or S as it is.
+#pragma unroll
+  for (int f = 0; f < 2; ++f)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int n = n0 + 32 * (2 * wn + f) + 8 * j + 4 * (lane >> 5);
+      float bv[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+      if constexpr (HAS_BIAS && EPI == Epilogue::kBf16) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          bv[r] = __uint_as_float(static_cast<uint32_t>(bias[min(n + r, N - 1)]) << 16);
+      }
+#pragma unroll
+      for (int fb = 0; fb < 2; ++fb) {
+        const int m = m0 + 32 * (2 * wm + fb) + (lane & 31);
+        if (m >= M) continue;
+        if constexpr (EPI == Epilogue::kF32) {
+          float* p = static_cast<float*>(out) + static_cast<int64_t>(m) * N + n;
+          if (n + 3 < N && N % 4 == 0) {
+            *reinterpret_cast<float4*>(p) =
+                make_float4(S[f][fb][4 * j], S[f][fb][4 * j + 1], S[f][fb][4 * j + 2], S[f][fb][4 * j + 3]);
+          } else {
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+              if (n + r < N) p[r] = S[f][fb][4 * j + r];
+          }
+        } else {
+          uint16_t h[4];
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            float v = S[f][fb][4 * j + r];
+            if (HAS_BIAS) v = v + bv[r];
+            h[r] = __builtin_bit_cast(uint16_t, static_cast<__bf16>(v));
+          }
+          uint16_t* p = static_cast<uint16_t*>(out) + static_cast<int64_t>(m) * N + n;
+          if (n + 3 < N && N % 4 == 0) {
+            *reinterpret_cast<uint2*>(p) = make_uint2(h[0] | (static_cast<uint32_t>(h[1]) << 16),
+                                                      h[2] | (static_cast<uint32_t>(h[3]) << 16));
+          } else {
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+              if (n + r < N) p[r] = h[r];
+          }
+        }
+      }
+    }
+}
+
+template <int NJ, int G>
 hipError_t launch_qf6(const uint16_t* x, int64_t M, int64_t K, int64_t ksteps, uint8_t* out, float* s, int threads,
                       hipStream_t st) {
   const int64_t rows_padded = (M + 31) / 32 * 32;
   const int64_t groups_of_8_bands = (rows_padded / 32 + kNumXcd - 1) / kNumXcd;
   const dim3 grid(static_cast<unsigned>(groups_of_8_bands * 32 * kNumXcd));
   const size_t lds = static_cast<size_t>(threads / 64) * 256 * 16;
-  hipLaunchKernelGGL(quantize_rows_f6_kernel<NJ>, grid, dim3(threads), lds, st, x, M, K, rows_padded, ksteps, out, s);
+  hipLaunchKernelGGL((quantize_rows_f6_kernel<NJ, G>), grid, dim3(threads), lds, st, x, M, K, rows_padded, ksteps, out, s);
   return hipGetLastError();
 }
 
@@ -829,9 +1131,52 @@ hipError_t launch_quantize_rows_f6(const uint16_t* x, int64_t M, int64_t K, uint
   const int64_t threads = groups <= 512 ? (groups + 63) / 64 * 64 : 512;
   const int64_t nj = (groups + threads - 1) / threads;
   const int th = static_cast<int>(threads);
-  if (nj <= 1) return launch_qf6<1>(x, M, K, ksteps, out, scale, th, st);
-  if (nj <= 2) return launch_qf6<2>(x, M, K, ksteps, out, scale, th, st);
-  return launch_qf6<4>(x, M, K, ksteps, out, scale, th, st);
+  if (nj <= 1) return launch_qf6<1, 0>(x, M, K, ksteps, out, scale, th, st);
+  if (nj <= 2) return launch_qf6<2, 0>(x, M, K, ksteps, out, scale, th, st);
+  return launch_qf6<4, 0>(x, M, K, ksteps, out, scale, th, st);
+}
+
+hipError_t launch_quantize_groups_f6(const uint16_t* x, int64_t M, int64_t K, int G, uint8_t* out, float* scale,
+                                     hipStream_t st) {
+  const int64_t ksteps = f6_ksteps(K);
+  const int64_t groups = 2 * ksteps;
+  const int64_t threads = groups <= 512 ? (groups + 63) / 64 * 64 : 512;
+  const int64_t nj = (groups + threads - 1) / threads;
+  const int th = static_cast<int>(threads);
+  if (G == 64) {
+    if (nj <= 1) return launch_qf6<1, 64>(x, M, K, ksteps, out, scale, th, st);
+    if (nj <= 2) return launch_qf6<2, 64>(x, M, K, ksteps, out, scale, th, st);
+    return launch_qf6<4, 64>(x, M, K, ksteps, out, scale, th, st);
+  }
+  if (nj <= 1) return launch_qf6<1, 128>(x, M, K, ksteps, out, scale, th, st);
+  if (nj <= 2) return launch_qf6<2, 128>(x, M, K, ksteps, out, scale, th, st);
+  return launch_qf6<4, 128>(x, M, K, ksteps, out, scale, th, st);
+}
+
+hipError_t launch_w4a4g_f6_gemm(Epilogue epi, const uint8_t* xf6, const float* sx, int64_t M, int64_t K, int G,
+                                const uint8_t* wf6, const float* sw, int64_t N, const uint16_t* bias, void* out,
+                                hipStream_t st) {
+  const int ksteps = static_cast<int>(f6_ksteps(K));
+  const int tiles_m = static_cast<int>((M + 127) / 128), tiles_n = static_cast<int>((N + 127) / 128);
+  const int64_t tiles = static_cast<int64_t>(tiles_m) * tiles_n;
+  const unsigned blocks = static_cast<unsigned>((tiles + kNumXcd - 1) / kNumXcd * kNumXcd);
+  const int mbands = static_cast<int>((M + 31) / 32), nbands = static_cast<int>((N + 31) / 32);
+  const int KG = static_cast<int>(K / G);
+  const int Mi = static_cast<int>(M), Ni = static_cast<int>(N);
+#define JQ_F6G(GG, E, B)                                                                                       \
+  hipLaunchKernelGGL((w4a4g_f6_gemm_kernel<GG, E, B>), dim3(blocks), dim3(256), 0, st, xf6, sx, Mi, mbands, wf6, \
+                     sw, Ni, nbands, ksteps, KG, bias, out, tiles_m, tiles_n)
+  if (G == 64) {
+    if (epi == Epilogue::kF32) JQ_F6G(64, Epilogue::kF32, false);
+    else if (bias != nullptr) JQ_F6G(64, Epilogue::kBf16, true);
+    else JQ_F6G(64, Epilogue::kBf16, false);
+  } else {
+    if (epi == Epilogue::kF32) JQ_F6G(128, Epilogue::kF32, false);
+    else if (bias != nullptr) JQ_F6G(128, Epilogue::kBf16, true);
+    else JQ_F6G(128, Epilogue::kBf16, false);
+  }
+#undef JQ_F6G
+  return hipGetLastError();
 }
 
 hipError_t launch_int4_to_f6(const uint8_t* q, int64_t rows, int64_t K, uint8_t* out, bool weight_layout,

@@ -319,6 +319,29 @@ size_t f6_workspace_bytes(int64_t M, int64_t K) {
          round_up(static_cast<size_t>(M) * sizeof(float), kWsAlign);
 }
 
+jq_status check_group_f6_gemm(const void* xf6, const float* sx, int64_t M, int64_t K, int64_t G, const void* wf6,
+                              const float* sw, int64_t N, const void* bias, const void* y) {
+  if (xf6 == nullptr || wf6 == nullptr || y == nullptr || sx == nullptr || sw == nullptr) return JQ_ERR_INVALID_ARG;
+  jq_status st = check_group(M, K, G);
+  if (st != JQ_OK) return st;
+  st = check_group(N, K, G);
+  if (st != JQ_OK) return st;
+  st = check_f6_operands(M, N, K);
+  if (st != JQ_OK) return st;
+  // 32-bit tile indices over 128 x 128 tiles
+  if (((M + 127) / 128) * ((N + 127) / 128) > (int64_t(1) << 26)) return JQ_ERR_UNSUPPORTED_SHAPE;
+  if (!aligned(xf6, 16) || !aligned(wf6, 16) || !aligned(y, 16)) return JQ_ERR_MISALIGNED;
+  if (!aligned(sx, 4) || !aligned(sw, 4)) return JQ_ERR_MISALIGNED;
+  if (bias != nullptr && !aligned(bias, 2)) return JQ_ERR_MISALIGNED;
+  return JQ_OK;
+}
+
+size_t group_f6_workspace_bytes(int64_t M, int64_t K, int64_t G) {
+  if (check_group(M, K, G) != JQ_OK) return 0;
+  return round_up(static_cast<size_t>(jq::f6_operand_bytes(M, K)), kWsAlign) +
+         round_up(static_cast<size_t>(M) * static_cast<size_t>(K / G) * sizeof(float), kWsAlign);
+}
+
 }  // namespace
 
 extern "C" {
@@ -401,6 +424,56 @@ jq_status jq_w4a4_f6_gemm_i32(const void* xf6, int64_t M, int64_t K, const void*
   return from_hip(jq::launch_w4a4_f6_gemm(jq::Epilogue::kInt32, static_cast<const uint8_t*>(xf6), nullptr, M, K,
                                           static_cast<const uint8_t*>(wf6), nullptr, N, nullptr, acc,
                                           as_stream(stream)));
+}
+
+
+jq_status jq_quantize_act_group_f6(const void* x_bf16, int64_t M, int64_t K, int64_t G, void* xf6, float* scales,
+                                   void* stream) {
+  if (x_bf16 == nullptr || xf6 == nullptr || scales == nullptr) return JQ_ERR_INVALID_ARG;
+  const jq_status st = check_group(M, K, G);
+  if (st != JQ_OK) return st;
+  if (!aligned(x_bf16, 16) || !aligned(xf6, 16) || !aligned(scales, 4)) return JQ_ERR_MISALIGNED;
+  return from_hip(jq::launch_quantize_groups_f6(static_cast<const uint16_t*>(x_bf16), M, K, static_cast<int>(G),
+                                                static_cast<uint8_t*>(xf6), scales, as_stream(stream)));
+}
+
+size_t jq_w4a4g_f6_workspace_bytes(int64_t M, int64_t K, int64_t G) { return group_f6_workspace_bytes(M, K, G); }
+
+jq_status jq_w4a4g_f6_linear(const void* x_bf16, int64_t M, int64_t K, int64_t G, const void* wf6,
+                             const float* w_scales, int64_t N, const void* bias_bf16, void* y_bf16, void* workspace,
+                             size_t workspace_bytes, void* stream) {
+  if (x_bf16 == nullptr || workspace == nullptr) return JQ_ERR_INVALID_ARG;
+  // the activation operand lives in the workspace; check the rest with stand-ins
+  const jq_status st = check_group_f6_gemm(x_bf16, w_scales, M, K, G, wf6, w_scales, N, bias_bf16, y_bf16);
+  if (st != JQ_OK) return st;
+  if (!aligned(workspace, kWsAlign)) return JQ_ERR_MISALIGNED;
+  if (workspace_bytes < group_f6_workspace_bytes(M, K, G)) return JQ_ERR_WORKSPACE_TOO_SMALL;
+  uint8_t* xf6 = static_cast<uint8_t*>(workspace);
+  float* sx = reinterpret_cast<float*>(xf6 + round_up(static_cast<size_t>(jq::f6_operand_bytes(M, K)), kWsAlign));
+  hipError_t e = jq::launch_quantize_groups_f6(static_cast<const uint16_t*>(x_bf16), M, K, static_cast<int>(G), xf6,
+                                               sx, as_stream(stream));
+  if (e != hipSuccess) return JQ_ERR_HIP;
+  return from_hip(jq::launch_w4a4g_f6_gemm(jq::Epilogue::kBf16, xf6, sx, M, K, static_cast<int>(G),
+                                           static_cast<const uint8_t*>(wf6), w_scales, N,
+                                           static_cast<const uint16_t*>(bias_bf16), y_bf16, as_stream(stream)));
+}
+
+jq_status jq_w4a4g_f6_gemm(const void* xf6, const float* scales, int64_t M, int64_t K, int64_t G, const void* wf6,
+                           const float* w_scales, int64_t N, const void* bias_bf16, void* y_bf16, void* stream) {
+  const jq_status st = check_group_f6_gemm(xf6, scales, M, K, G, wf6, w_scales, N, bias_bf16, y_bf16);
+  if (st != JQ_OK) return st;
+  return from_hip(jq::launch_w4a4g_f6_gemm(jq::Epilogue::kBf16, static_cast<const uint8_t*>(xf6), scales, M, K,
+                                           static_cast<int>(G), static_cast<const uint8_t*>(wf6), w_scales, N,
+                                           static_cast<const uint16_t*>(bias_bf16), y_bf16, as_stream(stream)));
+}
+
+jq_status jq_w4a4g_f6_gemm_f32(const void* xf6, const float* scales, int64_t M, int64_t K, int64_t G,
+                               const void* wf6, const float* w_scales, int64_t N, float* s_f32, void* stream) {
+  const jq_status st = check_group_f6_gemm(xf6, scales, M, K, G, wf6, w_scales, N, nullptr, s_f32);
+  if (st != JQ_OK) return st;
+  return from_hip(jq::launch_w4a4g_f6_gemm(jq::Epilogue::kF32, static_cast<const uint8_t*>(xf6), scales, M, K,
+                                           static_cast<int>(G), static_cast<const uint8_t*>(wf6), w_scales, N,
+                                           nullptr, s_f32, as_stream(stream)));
 }
 
 }  // extern "C"

@@ -59,6 +59,15 @@ int f6_tile_bands(int64_t M, int64_t N, int64_t slots);
 hipError_t launch_quantize_rows_f6(const uint16_t* x, int64_t M, int64_t K, uint8_t* out, float* scale,
                                    hipStream_t st);
 
+// Group-wise BF6 engine (G = 64 or 128): the group quantiser writing the BF6
+// activation operand and scales [M, K/G]; the group GEMM on BF6 operands with
+// scales [M, K/G] and [N, K/G] (epi kBf16 or kF32).
+hipError_t launch_quantize_groups_f6(const uint16_t* x, int64_t M, int64_t K, int G, uint8_t* out, float* scale,
+                                     hipStream_t st);
+hipError_t launch_w4a4g_f6_gemm(Epilogue epi, const uint8_t* xf6, const float* sx, int64_t M, int64_t K, int G,
+                                const uint8_t* wf6, const float* sw, int64_t N, const uint16_t* bias, void* out,
+                                hipStream_t st);
+
 // Canonical packed int4 codes ([rows, K/2]) or packed ternary codes
 // ([rows, K/4], `ternary`) -> BF6 operand in the activation layout or the
 // weight layout (padding written as zeros).

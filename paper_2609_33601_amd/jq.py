@@ -49,6 +49,11 @@ SIGNATURES = {
     "jq_w4a4_f6_linear": (ctypes.c_int, [_vp, _i64, _i64, _vp, _fp, _i64, _vp, _vp, _vp, _sz, _vp]),
     "jq_w4a4_f6_gemm": (ctypes.c_int, [_vp, _fp, _i64, _i64, _vp, _fp, _i64, _vp, _vp, _vp]),
     "jq_w4a4_f6_gemm_i32": (ctypes.c_int, [_vp, _i64, _i64, _vp, _i64, _ip, _vp]),
+    "jq_quantize_act_group_f6": (ctypes.c_int, [_vp, _i64, _i64, _i64, _vp, _fp, _vp]),
+    "jq_w4a4g_f6_workspace_bytes": (ctypes.c_size_t, [_i64, _i64, _i64]),
+    "jq_w4a4g_f6_linear": (ctypes.c_int, [_vp, _i64, _i64, _i64, _vp, _fp, _i64, _vp, _vp, _vp, _sz, _vp]),
+    "jq_w4a4g_f6_gemm": (ctypes.c_int, [_vp, _fp, _i64, _i64, _i64, _vp, _fp, _i64, _vp, _vp, _vp]),
+    "jq_w4a4g_f6_gemm_f32": (ctypes.c_int, [_vp, _fp, _i64, _i64, _i64, _vp, _fp, _i64, _fp, _vp]),
 }
 
 _lib = None
@@ -489,3 +494,84 @@ def bf16_bits(t):
 
     torch = _torch()
     return t.detach().contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+
+
+# ---------------------------------------------------------------------------
+# group-wise W4A4 on the BF6 engine: BF6 operands, scales [rows, K/G]
+# ---------------------------------------------------------------------------
+
+
+def jq_w4a4g_f6_workspace_bytes(M, K, G):
+    return int(lib().jq_w4a4g_f6_workspace_bytes(int(M), int(K), int(G)))
+
+
+def jq_quantize_act_group_f6(x, G, xf6=None, scale=None, stream=None):
+    """x bf16 [M,K] -> (BF6 activation operand uint8 [jq_f6_operand_bytes(M,K)], scales fp32 [M,K/G])."""
+    torch = _torch()
+    M, K = x.shape
+    nb = jq_f6_operand_bytes(M, K)
+    if xf6 is None:
+        xf6 = torch.empty((nb,), dtype=torch.uint8, device=x.device)
+    if scale is None:
+        scale = torch.empty((M, K // G), dtype=torch.float32, device=x.device)
+    st = lib().jq_quantize_act_group_f6(_dev(x, torch.bfloat16, None, "x"), M, K, G,
+                                        _dev(xf6, torch.uint8, (nb,), "xf6"),
+                                        _dev(scale, torch.float32, (M, K // G), "scale"), _stream_ptr(stream))
+    _check(st, "jq_quantize_act_group_f6")
+    return xf6, scale
+
+
+def jq_w4a4g_f6_linear(x, wf6, w_scale, G, bias=None, y=None, workspace=None, stream=None):
+    """y = group-wise W4A4 linear of x (bf16 [M,K]) on the BF6 engine; wf6 from
+    jq_int4_to_f6_weight of jq_pack_weight_int4_group's codes, w_scale its scales [N,K/G]."""
+    torch = _torch()
+    M, K = x.shape
+    N = w_scale.shape[0]
+    if y is None:
+        y = torch.empty((M, N), dtype=torch.bfloat16, device=x.device)
+    if workspace is None:
+        workspace = torch.empty((jq_w4a4g_f6_workspace_bytes(M, K, G),), dtype=torch.uint8, device=x.device)
+    bptr = ctypes.c_void_p(None) if bias is None else _dev(bias, torch.bfloat16, (N,), "bias")
+    st = lib().jq_w4a4g_f6_linear(_dev(x, torch.bfloat16, None, "x"), M, K, G,
+                                  _dev(wf6, torch.uint8, (jq_f6_operand_bytes(N, K),), "wf6"),
+                                  _dev(w_scale, torch.float32, (N, K // G), "w_scale"), N, bptr,
+                                  _dev(y, torch.bfloat16, (M, N), "y"),
+                                  _dev(workspace, torch.uint8, None, "workspace"), workspace.numel(),
+                                  _stream_ptr(stream))
+    _check(st, "jq_w4a4g_f6_linear")
+    return y
+
+
+def jq_w4a4g_f6_gemm(xf6, scale, wf6, w_scale, G, bias=None, y=None, stream=None):
+    """Group GEMM + epilogue on the BF6 engine (scale [M,K/G], w_scale [N,K/G]); returns bf16 [M,N]."""
+    torch = _torch()
+    M, KG = scale.shape
+    N = w_scale.shape[0]
+    K = KG * G
+    if y is None:
+        y = torch.empty((M, N), dtype=torch.bfloat16, device=xf6.device)
+    bptr = ctypes.c_void_p(None) if bias is None else _dev(bias, torch.bfloat16, (N,), "bias")
+    st = lib().jq_w4a4g_f6_gemm(_dev(xf6, torch.uint8, (jq_f6_operand_bytes(M, K),), "xf6"),
+                                _dev(scale, torch.float32, (M, KG), "scale"), M, K, G,
+                                _dev(wf6, torch.uint8, (jq_f6_operand_bytes(N, K),), "wf6"),
+                                _dev(w_scale, torch.float32, (N, KG), "w_scale"), N, bptr,
+                                _dev(y, torch.bfloat16, (M, N), "y"), _stream_ptr(stream))
+    _check(st, "jq_w4a4g_f6_gemm")
+    return y
+
+
+def jq_w4a4g_f6_gemm_f32(xf6, scale, wf6, w_scale, G, out=None, stream=None):
+    """The fp32 group sum S [M,N] of the BF6 group GEMM (before bias and bf16 rounding)."""
+    torch = _torch()
+    M, KG = scale.shape
+    N = w_scale.shape[0]
+    K = KG * G
+    if out is None:
+        out = torch.empty((M, N), dtype=torch.float32, device=xf6.device)
+    st = lib().jq_w4a4g_f6_gemm_f32(_dev(xf6, torch.uint8, (jq_f6_operand_bytes(M, K),), "xf6"),
+                                    _dev(scale, torch.float32, (M, KG), "scale"), M, K, G,
+                                    _dev(wf6, torch.uint8, (jq_f6_operand_bytes(N, K),), "wf6"),
+                                    _dev(w_scale, torch.float32, (N, KG), "w_scale"), N,
+                                    _dev(out, torch.float32, (M, N), "out"), _stream_ptr(stream))
+    _check(st, "jq_w4a4g_f6_gemm_f32")
+    return out

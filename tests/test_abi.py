@@ -31,7 +31,7 @@ def header_functions():
 
 def test_exports_every_declared_symbol():
     names = header_functions()
-    assert len(names) == 27, names
+    assert len(names) == 32, names
     lib = ctypes.CDLL(jq.LIB_PATH)
     for n in names:
         assert hasattr(lib, n), f"libjq.so does not export {n}"
@@ -232,3 +232,30 @@ def test_f6_gemm_and_linear_validation():
     assert L.jq_w4a4_f6_gemm_i32(A, 8, 64, A, 8, MIS, None) == jq.JQ_ERR_MISALIGNED
     # operands of 2 GiB or more are refused (31-bit buffer descriptors)
     assert L.jq_w4a4_f6_gemm_i32(A, 1 << 22, 65536, A, 8, A, None) == jq.JQ_ERR_UNSUPPORTED_SHAPE
+
+
+def test_group_f6_validation():
+    L = jq.lib()
+    # workspace: BF6 operand + scales, each rounded up to 256 bytes; 0 for invalid sizes
+    assert L.jq_w4a4g_f6_workspace_bytes(8, 128, 64) == L.jq_f6_operand_bytes(8, 128) + 256
+    assert L.jq_w4a4g_f6_workspace_bytes(8, 128, 32) == 0
+    assert L.jq_w4a4g_f6_workspace_bytes(8, 192, 128) == 0
+    assert L.jq_quantize_act_group_f6(None, 8, 128, 64, A, A, None) == jq.JQ_ERR_INVALID_ARG
+    assert L.jq_quantize_act_group_f6(A, 8, 128, 96, A, A, None) == jq.JQ_ERR_UNSUPPORTED_SHAPE
+    assert L.jq_quantize_act_group_f6(A, 8, 192, 128, A, A, None) == jq.JQ_ERR_UNSUPPORTED_SHAPE
+    assert L.jq_quantize_act_group_f6(A, 8, 128, 64, MIS, A, None) == jq.JQ_ERR_MISALIGNED
+    assert L.jq_quantize_act_group_f6(A, 8, 128, 64, A, A + 1, None) == jq.JQ_ERR_MISALIGNED
+    ws = L.jq_w4a4g_f6_workspace_bytes(8, 128, 64)
+    assert L.jq_w4a4g_f6_linear(None, 8, 128, 64, A, A, 8, None, A, A, ws, None) == jq.JQ_ERR_INVALID_ARG
+    assert L.jq_w4a4g_f6_linear(A, 8, 128, 64, A, A, 8, None, A, A, ws - 1, None) == jq.JQ_ERR_WORKSPACE_TOO_SMALL
+    assert L.jq_w4a4g_f6_linear(A, 8, 128, 64, A, A, 8, None, A, A + 16, ws, None) == jq.JQ_ERR_MISALIGNED
+    assert L.jq_w4a4g_f6_linear(A, 8, 128, 64, A, None, 8, None, A, A, ws, None) == jq.JQ_ERR_INVALID_ARG
+    assert L.jq_w4a4g_f6_gemm(A, None, 8, 128, 64, A, A, 8, None, A, None) == jq.JQ_ERR_INVALID_ARG
+    assert L.jq_w4a4g_f6_gemm(A, A, 8, 128, 48, A, A, 8, None, A, None) == jq.JQ_ERR_UNSUPPORTED_SHAPE
+    assert L.jq_w4a4g_f6_gemm(A, A, 8, 128, 64, A, A, 0, None, A, None) == jq.JQ_ERR_INVALID_ARG
+    assert L.jq_w4a4g_f6_gemm(A, A, 8, 128, 64, A, A, 8, A + 1, A, None) == jq.JQ_ERR_MISALIGNED
+    assert L.jq_w4a4g_f6_gemm(A, A, 8, 128, 64, MIS, A, 8, None, A, None) == jq.JQ_ERR_MISALIGNED
+    assert L.jq_w4a4g_f6_gemm_f32(A, A, 8, 128, 64, A, A, 8, None, None) == jq.JQ_ERR_INVALID_ARG
+    assert L.jq_w4a4g_f6_gemm_f32(A, A, 8, 128, 64, A, A, 8, MIS, None) == jq.JQ_ERR_MISALIGNED
+    # operands of 2 GiB or more are refused (31-bit buffer descriptors)
+    assert L.jq_w4a4g_f6_gemm_f32(A, A, 1 << 22, 65536, 64, A, A, 8, A, None) == jq.JQ_ERR_UNSUPPORTED_SHAPE
