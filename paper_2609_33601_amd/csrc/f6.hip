@@ -1026,23 +1026,17 @@ __global__ __launch_bounds__(256, 2) void w4a4g_f6_gemm_kernel(
     compute(u + 1, 1);
   }
 
-  // Epilogue: bias (bf16) added in fp32, rounded to bf16; or S as it is.
+  if constexpr (EPI == Epilogue::kF32) {
+    // S as it is (the checking path): four consecutive n per store.
 #pragma unroll
-  for (int f = 0; f < 2; ++f)
+    for (int f = 0; f < 2; ++f)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int n = n0 + 32 * (2 * wn + f) + 8 * j + 4 * (lane >> 5);
-      float bv[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-      if constexpr (HAS_BIAS && EPI == Epilogue::kBf16) {
+      for (int j = 0; j < 4; ++j) {
+        const int n = n0 + 32 * (2 * wn + f) + 8 * j + 4 * (lane >> 5);
 #pragma unroll
-        for (int r = 0; r < 4; ++r)
-          bv[r] = __uint_as_float(static_cast<uint32_t>(bias[min(n + r, N - 1)]) << 16);
-      }
-#pragma unroll
-      for (int fb = 0; fb < 2; ++fb) {
-        const int m = m0 + 32 * (2 * wm + fb) + (lane & 31);
-        if (m >= M) continue;
-        if constexpr (EPI == Epilogue::kF32) {
+        for (int fb = 0; fb < 2; ++fb) {
+          const int m = m0 + 32 * (2 * wm + fb) + (lane & 31);
+          if (m >= M) continue;
           float* p = static_cast<float*>(out) + static_cast<int64_t>(m) * N + n;
           if (n + 3 < N && N % 4 == 0) {
             *reinterpret_cast<float4*>(p) =
@@ -1052,26 +1046,66 @@ __global__ __launch_bounds__(256, 2) void w4a4g_f6_gemm_kernel(
             for (int r = 0; r < 4; ++r)
               if (n + r < N) p[r] = S[f][fb][4 * j + r];
           }
-        } else {
+        }
+      }
+  } else {
+    // bf16(S + bias), staged through LDS (the first slot, free once every
+    // wave is past the last stage) and stored as whole 128-byte rows: per
+    // wave two passes of 32 rows x 64 columns, 16-byte chunk c of row r at
+    // chunk c ^ ((r >> 1) & 7).
+    __syncthreads();
+    v4u32* stg = reinterpret_cast<v4u32*>(op0) + 256 * wave;
+    v2u32* stg2 = reinterpret_cast<v2u32*>(stg);
+    float bv[2][4][4];
+#pragma unroll
+    for (int f = 0; f < 2; ++f)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int n = n0 + 32 * (2 * wn + f) + 8 * j + 4 * (lane >> 5) + r;
+          bv[f][j][r] = HAS_BIAS ? __uint_as_float(static_cast<uint32_t>(bias[min(n, N - 1)]) << 16) : 0.0f;
+        }
+    const bool vec = (n0 + 128 <= N) && (N % 8 == 0);
+#pragma unroll
+    for (int fb = 0; fb < 2; ++fb) {
+      const int row = lane & 31;
+#pragma unroll
+      for (int f = 0; f < 2; ++f)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int c = 32 * f + 8 * j + 4 * (lane >> 5);  // column within the wave's 64
           uint16_t h[4];
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
             float v = S[f][fb][4 * j + r];
-            if (HAS_BIAS) v = v + bv[r];
+            if (HAS_BIAS) v = v + bv[f][j][r];
             h[r] = __builtin_bit_cast(uint16_t, static_cast<__bf16>(v));
           }
-          uint16_t* p = static_cast<uint16_t*>(out) + static_cast<int64_t>(m) * N + n;
-          if (n + 3 < N && N % 4 == 0) {
-            *reinterpret_cast<uint2*>(p) = make_uint2(h[0] | (static_cast<uint32_t>(h[1]) << 16),
-                                                      h[2] | (static_cast<uint32_t>(h[3]) << 16));
-          } else {
+          stg2[2 * (8 * row + ((c >> 3) ^ ((row >> 1) & 7))) + ((c & 7) >> 2)] =
+              v2u32{h[0] | (static_cast<uint32_t>(h[1]) << 16), h[2] | (static_cast<uint32_t>(h[3]) << 16)};
+        }
+      __builtin_amdgcn_wave_barrier();
 #pragma unroll
-            for (int r = 0; r < 4; ++r)
-              if (n + r < N) p[r] = h[r];
-          }
+      for (int it = 0; it < 4; ++it) {
+        const int rr = 8 * it + (lane >> 3), ch = lane & 7;
+        const v4u32 vv = stg[8 * rr + (ch ^ ((rr >> 1) & 7))];
+        const int m = m0 + 32 * (2 * wm + fb) + rr;
+        const int n = n0 + 64 * wn + 8 * ch;
+        uint16_t* p = static_cast<uint16_t*>(out) + static_cast<int64_t>(m) * N + n;
+        if (m >= M) {
+        } else if (vec) {
+          *reinterpret_cast<uint4*>(p) = make_uint4(vv.x, vv.y, vv.z, vv.w);
+        } else {
+          const uint32_t w[4] = {vv.x, vv.y, vv.z, vv.w};
+#pragma unroll
+          for (int e = 0; e < 8; ++e)
+            if (n + e < N) p[e] = static_cast<uint16_t>(w[e >> 1] >> (16 * (e & 1)));
         }
       }
+      __builtin_amdgcn_wave_barrier();
     }
+  }
 }
 
 template <int NJ, int G>
