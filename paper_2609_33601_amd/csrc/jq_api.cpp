@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <algorithm>
+
 #include "jq.h"
 #include "jq_internal.h"
 
@@ -474,6 +476,16 @@ jq_status jq_w4a4g_f6_gemm_f32(const void* xf6, const float* scales, int64_t M, 
   return from_hip(jq::launch_w4a4g_f6_gemm(jq::Epilogue::kF32, static_cast<const uint8_t*>(xf6), scales, M, K,
                                            static_cast<int>(G), static_cast<const uint8_t*>(wf6), w_scales, N,
                                            nullptr, s_f32, as_stream(stream)));
+}
+
+jq_status jq_f6_gemm_plan(int64_t M, int64_t N, int64_t K, int cus, int* waves, int* tile_rows) {
+  if (waves == nullptr || tile_rows == nullptr || cus < 1) return JQ_ERR_INVALID_ARG;
+  const jq_status st = check_f6_operands(M, N, K);
+  if (st != JQ_OK) return st;
+  const int64_t slots = std::max<int64_t>(8, cus / 8 * 8);
+  *waves = jq::f6_block_waves(M, N, K, slots);
+  *tile_rows = 32 * (*waves == 4 ? 4 : jq::f6_tile_bands(M, N, slots));
+  return JQ_OK;
 }
 
 }  // extern "C"

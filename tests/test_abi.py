@@ -31,7 +31,7 @@ def header_functions():
 
 def test_exports_every_declared_symbol():
     names = header_functions()
-    assert len(names) == 32, names
+    assert len(names) == 33, names
     lib = ctypes.CDLL(jq.LIB_PATH)
     for n in names:
         assert hasattr(lib, n), f"libjq.so does not export {n}"
@@ -259,3 +259,21 @@ def test_group_f6_validation():
     assert L.jq_w4a4g_f6_gemm_f32(A, A, 8, 128, 64, A, A, 8, MIS, None) == jq.JQ_ERR_MISALIGNED
     # operands of 2 GiB or more are refused (31-bit buffer descriptors)
     assert L.jq_w4a4g_f6_gemm_f32(A, A, 1 << 22, 65536, 64, A, A, 8, A, None) == jq.JQ_ERR_UNSUPPORTED_SHAPE
+
+
+def test_f6_gemm_plan():
+    """The BF6 GEMM's block shape: one 8-wave block per CU where 256-row tiles
+    cover M evenly or K is long, two 4-wave blocks (128-row tiles) otherwise."""
+    plan = lambda M, N, K: jq.jq_f6_gemm_plan(M, N, K, 256)
+    assert plan(4608, 12288, 3072) == (4, 128)    # FLUX MLP-up: 224-row tiles would not cover M evenly
+    assert plan(9216, 3072, 12288) == (8, 224)    # FLUX MLP-down: long K
+    assert plan(4096, 12288, 4096) == (8, 256)    # dLLM gate/up: 256-row tiles fit exactly
+    assert plan(4096, 4096, 12288) == (8, 256)    # dLLM down
+    assert plan(4608, 3072, 3072) == (4, 128)     # DiT attention projection
+    assert plan(4608, 3072, 8192) == (8, 224)     # K above 6144 keeps the 8-wave block
+    assert plan(64, 256, 256) == (4, 128)         # small shapes
+    L = jq.lib()
+    w, t = ctypes.c_int(), ctypes.c_int()
+    assert L.jq_f6_gemm_plan(8, 8, 64, 0, ctypes.byref(w), ctypes.byref(t)) == jq.JQ_ERR_INVALID_ARG
+    assert L.jq_f6_gemm_plan(8, 8, 64, 256, None, ctypes.byref(t)) == jq.JQ_ERR_INVALID_ARG
+    assert L.jq_f6_gemm_plan(8, 8, 96, 256, ctypes.byref(w), ctypes.byref(t)) == jq.JQ_ERR_UNSUPPORTED_SHAPE
