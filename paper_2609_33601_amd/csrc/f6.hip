@@ -334,6 +334,143 @@ __global__ __launch_bounds__(512) void quantize_rows_f6_kernel(const uint16_t* _
   }
 }
 
+// First row of block b in the four-rows-per-block quantiser: the eight
+// blocks of a band are consecutive blocks of one XCD, so the lines of a
+// fragment that they write piecewise meet in one L2.
+__device__ __forceinline__ int64_t row0_of_block4(int64_t b) {
+  const int64_t x = b % kNumXcd, j = b / kNumXcd;
+  return 32 * (kNumXcd * (j / 8) + x) + 4 * (j % 8);
+}
+
+// The same quantiser for rows of up to 512 groups (K <= 16384), four rows
+// per block: lane l of a wave takes row l % 4 and group slot l / 4, so that
+// the four lanes of a group slot store the same fragment piece of four
+// consecutive rows, 64 (and 32) contiguous bytes, instead of four scattered
+// 16- and 8-byte pieces.  Wave w's j-th set of groups is the 16 groups from
+// 16 (W j + w) in each of the four rows: four 1 KiB loads of whole lines (one
+// per row), regrouped per lane through LDS (chunk q = 64 row + 4 slot +
+// quarter at slot q ^ ((q >> 6) & 3): conflict-free both ways).  Per-row
+// maxima meet by shuffles within a wave and through LDS across waves; group
+// maxima (G = 64, 128) by shuffles between the lanes of a group.  The scales
+// and codes are those of quantize_rows_f6_kernel.
+template <int NJ, int G>
+__global__ __launch_bounds__(512) void quantize_rows4_f6_kernel(const uint16_t* __restrict__ x, int64_t M, int64_t K,
+                                                                int64_t rows_padded, int64_t ksteps,
+                                                                uint8_t* __restrict__ out, float* __restrict__ scale) {
+  __shared__ uint32_t wave_max[8][4];
+  const int T = blockDim.x;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nwaves = T >> 6;
+  const int64_t row0 = row0_of_block4(blockIdx.x);
+  if (row0 >= rows_padded) return;
+  const int rr = lane & 3, gslot = lane >> 2;
+  const int64_t row = row0 + rr;
+  const bool live = row < M;
+  const int groups = static_cast<int>(2 * ksteps);
+
+  extern __shared__ v4u32 xt[];  // 256 chunks of 16 bytes per wave
+  v4u32* xw = xt + 256 * wave;
+  auto swz = [](int q) { return q ^ ((q >> 6) & 3); };
+  // All loads first (NJ x 4 of them in flight), then the regrouping.
+  v4u32 t[NJ][4];
+#pragma unroll
+  for (int j = 0; j < NJ; ++j) {
+    const int g0 = 16 * (nwaves * j + wave);
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      // row row0 + c, elements 32 g0 + 8 lane .. + 7; out-of-range chunks load
+      // the first chunk of x and are zeroed (no branch between the loads)
+      const int64_t e = 32 * static_cast<int64_t>(g0) + 8 * lane;
+      const bool ok = row0 + c < M && e < K;
+      t[j][c] = __builtin_nontemporal_load(reinterpret_cast<const v4u32*>(ok ? x + (row0 + c) * K + e : x));
+      if (!ok) t[j][c] = v4u32{0, 0, 0, 0};
+    }
+  }
+  uint4 v[NJ][4];
+#pragma unroll
+  for (int j = 0; j < NJ; ++j) {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+#pragma unroll
+    for (int c = 0; c < 4; ++c) xw[swz(64 * c + lane)] = t[j][c];
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const v4u32 r = xw[swz(64 * rr + 4 * gslot + c)];
+      v[j][c] = make_uint4(r.x, r.y, r.z, r.w);
+    }
+  }
+  // The lane's maximum over each of its groups.
+  uint32_t gmax[NJ];
+#pragma unroll
+  for (int j = 0; j < NJ; ++j) {
+    u16x2 gm = {0, 0};
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      gm = __builtin_elementwise_max(gm, __builtin_bit_cast(u16x2, v[j][c].x & 0x7FFF7FFFu));
+      gm = __builtin_elementwise_max(gm, __builtin_bit_cast(u16x2, v[j][c].y & 0x7FFF7FFFu));
+      gm = __builtin_elementwise_max(gm, __builtin_bit_cast(u16x2, v[j][c].z & 0x7FFF7FFFu));
+      gm = __builtin_elementwise_max(gm, __builtin_bit_cast(u16x2, v[j][c].w & 0x7FFF7FFFu));
+    }
+    gmax[j] = gm.x > gm.y ? gm.x : gm.y;
+  }
+  float srow = 0.0f;
+  if constexpr (G == 0) {
+    uint32_t amax = 0;
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) amax = amax > gmax[j] ? amax : gmax[j];
+#pragma unroll
+    for (int off = 4; off <= 32; off <<= 1) {  // the 16 lanes of this row
+      const uint32_t o = static_cast<uint32_t>(__shfl_xor(static_cast<int>(amax), off, 64));
+      amax = amax > o ? amax : o;
+    }
+    if (nwaves > 1) {
+      if (gslot == 0) wave_max[wave][rr] = amax;
+      __syncthreads();
+      amax = wave_max[0][rr];
+      for (int w = 1; w < nwaves; ++w) amax = amax > wave_max[w][rr] ? amax : wave_max[w][rr];
+    }
+    srow = __uint_as_float(amax << 16) / 7.0f;
+    if (live && wave == 0 && gslot == 0) scale[row] = srow;
+  } else {
+    (void)wave_max;
+  }
+#pragma unroll
+  for (int j = 0; j < NJ; ++j) {
+    float s = srow;
+    if constexpr (G != 0) {
+      constexpr int kLanes = G / 32;  // group slots per group, 4 lanes apart
+      uint32_t gm = gmax[j];
+#pragma unroll
+      for (int off = 4; off < 4 * kLanes; off <<= 1) {
+        const uint32_t o = static_cast<uint32_t>(__shfl_xor(static_cast<int>(gm), off, 64));
+        gm = gm > o ? gm : o;
+      }
+      s = __uint_as_float(gm << 16) / 7.0f;
+    }
+    const int gi = 16 * (nwaves * j + wave) + gslot;
+    if (gi >= groups) continue;
+    if constexpr (G != 0) {
+      constexpr int kLanes = G / 32;
+      if (live && gi % kLanes == 0 && 32 * static_cast<int64_t>(gi) < K) scale[row * (K / G) + gi / kLanes] = s;
+    }
+    const float rcp = (s == 0.0f) ? 0.0f : 1.0f / s;
+    float q[32];
+    if (s == 0.0f) {
+#pragma unroll
+      for (int p = 0; p < 32; ++p) q[p] = 0.0f;
+    } else {
+      const uint32_t w[16] = {v[j][0].x, v[j][0].y, v[j][0].z, v[j][0].w, v[j][1].x, v[j][1].y,
+                              v[j][1].z, v[j][1].w, v[j][2].x, v[j][2].y, v[j][2].z, v[j][2].w,
+                              v[j][3].x, v[j][3].y, v[j][3].z, v[j][3].w};
+      codes32(w, s, rcp, __builtin_isinf(rcp), q);
+    }
+    store_group<false>(out, ksteps, row, gi, bf6_group(q));
+  }
+}
+
 // Canonical packed int4 codes (TERNARY false) or packed ternary codes (true)
 // -> BF6 operand in the activation or the weight layout.  One thread per
 // (row, 32-code group) of the padded operand; padding rows and codes are
@@ -1108,6 +1245,19 @@ __global__ __launch_bounds__(256, 2) void w4a4g_f6_gemm_kernel(
   }
 }
 
+// Four rows per block, W waves of 16 group slots, NJ sets of groups each.
+template <int NJ, int G>
+hipError_t launch_q4f6(const uint16_t* x, int64_t M, int64_t K, int64_t ksteps, uint8_t* out, float* s, int waves,
+                       hipStream_t st) {
+  const int64_t rows_padded = (M + 31) / 32 * 32;
+  const int64_t groups_of_8_bands = (rows_padded / 32 + kNumXcd - 1) / kNumXcd;
+  const dim3 grid(static_cast<unsigned>(groups_of_8_bands * 8 * kNumXcd));
+  const size_t lds = static_cast<size_t>(waves) * 256 * 16;
+  hipLaunchKernelGGL((quantize_rows4_f6_kernel<NJ, G>), grid, dim3(64 * waves), lds, st, x, M, K, rows_padded, ksteps,
+                     out, s);
+  return hipGetLastError();
+}
+
 template <int NJ, int G>
 hipError_t launch_qf6(const uint16_t* x, int64_t M, int64_t K, int64_t ksteps, uint8_t* out, float* s, int threads,
                       hipStream_t st) {
@@ -1157,34 +1307,36 @@ int f6_block_waves(int64_t M, int64_t N, int64_t K, int64_t slots) {
   return K > kShortK || f6_tile_bands(M, N, slots) == 8 ? 8 : 4;
 }
 
-hipError_t launch_quantize_rows_f6(const uint16_t* x, int64_t M, int64_t K, uint8_t* out, float* scale,
-                                   hipStream_t st) {
+template <int G>
+hipError_t launch_quantize_f6(const uint16_t* x, int64_t M, int64_t K, uint8_t* out, float* scale, hipStream_t st) {
   const int64_t ksteps = f6_ksteps(K);
   const int64_t groups = 2 * ksteps;
-  // Up to 512 threads per row, each holding NJ groups of 32 codes.
-  const int64_t threads = groups <= 512 ? (groups + 63) / 64 * 64 : 512;
+  if (groups <= 512) {
+    // four rows per block: up to 8 waves of 16 group slots, NJ <= 4 sets each
+    const int64_t waves = std::min<int64_t>(8, (groups + 15) / 16);
+    const int64_t nj = (groups + 16 * waves - 1) / (16 * waves);
+    const int w = static_cast<int>(waves);
+    if (nj <= 1) return launch_q4f6<1, G>(x, M, K, ksteps, out, scale, w, st);
+    if (nj <= 2) return launch_q4f6<2, G>(x, M, K, ksteps, out, scale, w, st);
+    if (nj <= 3) return launch_q4f6<3, G>(x, M, K, ksteps, out, scale, w, st);
+    return launch_q4f6<4, G>(x, M, K, ksteps, out, scale, w, st);
+  }
+  // longer rows: one row per block, up to 512 threads each holding NJ groups
+  const int64_t threads = 512;
   const int64_t nj = (groups + threads - 1) / threads;
   const int th = static_cast<int>(threads);
-  if (nj <= 1) return launch_qf6<1, 0>(x, M, K, ksteps, out, scale, th, st);
-  if (nj <= 2) return launch_qf6<2, 0>(x, M, K, ksteps, out, scale, th, st);
-  return launch_qf6<4, 0>(x, M, K, ksteps, out, scale, th, st);
+  if (nj <= 2) return launch_qf6<2, G>(x, M, K, ksteps, out, scale, th, st);
+  return launch_qf6<4, G>(x, M, K, ksteps, out, scale, th, st);
+}
+
+hipError_t launch_quantize_rows_f6(const uint16_t* x, int64_t M, int64_t K, uint8_t* out, float* scale,
+                                   hipStream_t st) {
+  return launch_quantize_f6<0>(x, M, K, out, scale, st);
 }
 
 hipError_t launch_quantize_groups_f6(const uint16_t* x, int64_t M, int64_t K, int G, uint8_t* out, float* scale,
                                      hipStream_t st) {
-  const int64_t ksteps = f6_ksteps(K);
-  const int64_t groups = 2 * ksteps;
-  const int64_t threads = groups <= 512 ? (groups + 63) / 64 * 64 : 512;
-  const int64_t nj = (groups + threads - 1) / threads;
-  const int th = static_cast<int>(threads);
-  if (G == 64) {
-    if (nj <= 1) return launch_qf6<1, 64>(x, M, K, ksteps, out, scale, th, st);
-    if (nj <= 2) return launch_qf6<2, 64>(x, M, K, ksteps, out, scale, th, st);
-    return launch_qf6<4, 64>(x, M, K, ksteps, out, scale, th, st);
-  }
-  if (nj <= 1) return launch_qf6<1, 128>(x, M, K, ksteps, out, scale, th, st);
-  if (nj <= 2) return launch_qf6<2, 128>(x, M, K, ksteps, out, scale, th, st);
-  return launch_qf6<4, 128>(x, M, K, ksteps, out, scale, th, st);
+  return G == 64 ? launch_quantize_f6<64>(x, M, K, out, scale, st) : launch_quantize_f6<128>(x, M, K, out, scale, st);
 }
 
 hipError_t launch_w4a4g_f6_gemm(Epilogue epi, const uint8_t* xf6, const float* sx, int64_t M, int64_t K, int G,
