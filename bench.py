@@ -225,7 +225,7 @@ def secondary(torch, jq, workloads, steps):
     out = []
     for wl, fmt in cases:
         preps = [Prepared(lin, torch, jq, fmt) for lin in wl.linears]
-        us = time_step(torch, preps, steps, warmup=5)
+        us = time_step(torch, preps, steps, warmup=20)
         tops = wl.ops / (us * 1e-6) / 1e12
         layer = {"ternary": "W1.58A4 (int8 engine)", "ternary_bf6": "W1.58A4 (bf6 engine)",
                  "int4": "W4A4 (int8 engine)", "bf6": "W4A4 (bf6 engine)",
