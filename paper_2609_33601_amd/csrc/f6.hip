@@ -13,10 +13,16 @@
 // Why it is faster.  gfx950 issues the 6-bit MFMA at twice the int8 rate, and the
 // operands reach it already encoded, so the loop holds no widening
 // arithmetic at all:
-//   * activations are quantised straight into BF6 by quantize_rows_f6_kernel
-//     (the same scale and codes as the packed-int4 quantiser);
+//   * activations are quantised straight into BF6 by quantize_rows4_f6_kernel
+//     (four rows per block) or quantize_rows_f6_kernel (longer rows), with
+//     the same scale and codes as the packed-int4 quantiser;
 //   * weights are converted once, offline, from the canonical packed int4
-//     codes.
+//     (or ternary) codes.
+//
+// The file also holds the group-wise form of the layer (one scale per G = 64
+// or 128 codes): the same quantisers with group scales, and
+// w4a4g_f6_gemm_kernel, which folds each group's exact product into fp32
+// sums in k order.
 //
 // BF6 groups.  32 codes c[0..31] form a group of 192 bits, code p in bits
 // 6p .. 6p+5 (six little-endian dwords d0..d5).  Rows are padded with zero
