@@ -149,6 +149,27 @@ class Prepared:
         self.s = torch.empty((lin.M,), dtype=torch.float32, device="cuda")
         if fmt in ("bf6", "ternary_bf6"):
             self.q = torch.empty((jq.jq_f6_operand_bytes(lin.M, lin.K),), dtype=torch.uint8, device="cuda")
+        # The layer split in two, for linears that share their input (the
+        # dLLM block's gate and up): quantise once, then one GEMM per linear.
+        K, q, s, b, y, wq, sw = lin.K, self.q, self.s, self.b, self.y, self.wq, self.sw
+        if fmt.startswith("group"):
+            G = int(fmt[5:-4]) if fmt.endswith("_bf6") else int(fmt[5:])
+            self.s = s = torch.empty((lin.M, lin.K // G), dtype=torch.float32, device="cuda")
+            if fmt.endswith("_bf6"):
+                self.q = q = torch.empty((jq.jq_f6_operand_bytes(lin.M, lin.K),), dtype=torch.uint8, device="cuda")
+                self.quantize = lambda: jq.jq_quantize_act_group_f6(self.x, G, xf6=q, scale=s)
+                self.gemm = lambda qq, ss: jq.jq_w4a4g_f6_gemm(qq, ss, wq, sw, G, b, y=y)
+            else:
+                self.quantize = lambda: jq.jq_quantize_act_group(self.x, G, q=q, scale=s)
+                self.gemm = lambda qq, ss: jq.jq_w4a4g_gemm(qq, ss, wq, sw, G, b, y=y)
+        elif fmt in ("bf6", "ternary_bf6"):
+            self.quantize = lambda: jq.jq_quantize_act_f6(self.x, xf6=q, scale=s)
+            self.gemm = lambda qq, ss: jq.jq_w4a4_f6_gemm(qq, ss, K, wq, sw, b, y=y)
+        else:
+            g = jq.jq_w158a4_gemm if fmt == "ternary" else jq.jq_w4a4_gemm
+            self.quantize = lambda: jq.jq_quantize_act(self.x, q=q, scale=s)
+            self.gemm = lambda qq, ss: g(qq, ss, wq, sw, b, y=y)
+        self.shares_input = False  # set for a linear whose input is the previous one's
 
 
 def cpu_baseline(preps, target_s):
@@ -194,12 +215,21 @@ def cpu_baseline(preps, target_s):
 
 
 def time_step(torch, preps, steps, warmup):
-    """Average time of one pass over the linears (each a whole quantise + GEMM layer), in us."""
+    """Average time of one pass over the linears (each a whole quantise + GEMM
+    layer; a linear that shares the previous one's input reuses its quantised
+    activations), in us."""
     stream = torch.cuda.current_stream()
 
     def step():
+        qs = None
         for p in preps:
-            p.linear(p.x, p.wq, p.sw, p.b, y=p.y, workspace=p.ws)
+            if p.shares_input and qs is not None:
+                p.gemm(*qs)
+            elif any(n.shares_input for n in preps):
+                qs = p.quantize()
+                p.gemm(*qs)
+            else:
+                p.linear(p.x, p.wq, p.sw, p.b, y=p.y, workspace=p.ws)
 
     for _ in range(warmup):
         step()
@@ -225,6 +255,8 @@ def secondary(torch, jq, workloads, steps):
     out = []
     for wl, fmt in cases:
         preps = [Prepared(lin, torch, jq, fmt) for lin in wl.linears]
+        for p in preps:
+            p.shares_input = p.lin.shares_input
         us = time_step(torch, preps, steps, warmup=20)
         tops = wl.ops / (us * 1e-6) / 1e12
         layer = {"ternary": "W1.58A4 (int8 engine)", "ternary_bf6": "W1.58A4 (bf6 engine)",

@@ -89,6 +89,8 @@ class Linear:
     w_seed: int
     bias_std: Optional[float] = None
     bias_seed: int = 2
+    # the input is the previous linear's (one quantisation serves both)
+    shares_input: bool = False
 
     @property
     def ops(self) -> int:
@@ -159,7 +161,7 @@ WORKLOADS = {
         "o-proj 4096x4096 -> 4096, down 4096x12288 -> 4096",
         (
             Linear("dllm_gate", N=12288, w_std=0.02, w_seed=1, **_dit_act(4096, 4096, seed=0)),
-            Linear("dllm_up", N=12288, w_std=0.02, w_seed=11, **_dit_act(4096, 4096, seed=0)),
+            Linear("dllm_up", N=12288, w_std=0.02, w_seed=11, shares_input=True, **_dit_act(4096, 4096, seed=0)),
             Linear("dllm_o", N=4096, w_std=0.02, w_seed=21, **_dit_act(4096, 4096, seed=0)),
             Linear("dllm_down", N=4096, w_std=0.02, w_seed=31, **_dit_act(4096, 12288, seed=10)),
         ),
