@@ -1,13 +1,19 @@
-"""Build libjq.so (the gfx950 HIP library behind include/jq.h) in-tree with hipcc."""
+"""Build libjq.so (the gfx950 HIP library behind include/jq.h) in-tree with hipcc.
+
+Each source compiles to its own object in parallel (_build/), then one hipcc
+link makes the shared library.  Every call compiles every source.
+"""
 
 import os
 import shutil
 import subprocess
 import sys
+from concurrent.futures import ThreadPoolExecutor
 
 PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
+OBJ_DIR = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libjq.so")
 SOURCES = ["quantize.hip", "ternary.hip", "gemm.hip", "gemm_group.hip", "f6.hip", "jq_api.cpp"]
 ARCH = "gfx950"
@@ -17,7 +23,6 @@ HIPCC_FLAGS = [
     "-O3",
     "-std=c++17",
     "-fPIC",
-    "-shared",
     # every fp32 operation of the quantiser and the epilogue is rounded on its own
     "-ffp-contract=off",
     # no packed-fp32 VALU instructions in device code
@@ -33,20 +38,31 @@ def hipcc():
     raise RuntimeError("hipcc not found: the HIP library cannot be built")
 
 
-def build(verbose=False, extra_flags=()):
-    """Compile the library; returns the path of the built .so."""
-    tmp = LIB + ".tmp"
-    cmd = [hipcc(), *HIPCC_FLAGS, *extra_flags,
-           "-I", os.path.join(ROOT, "include"), "-I", CSRC,
-           *[os.path.join(CSRC, s) for s in SOURCES], "-o", tmp]
+def _run(cmd, verbose):
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)
     out = "\n".join(l for l in res.stdout.splitlines() if "packed-fp32-ops" not in l)
     if res.returncode != 0:
-        raise RuntimeError(f"hipcc failed ({res.returncode}):\n{out}")
+        raise RuntimeError(f"hipcc failed ({res.returncode}): {' '.join(cmd)}\n{out}")
     if verbose and out.strip():
-        print(out)
+        print(out, flush=True)
+
+
+def build(verbose=False, extra_flags=(), jobs=None):
+    """Compile the library; returns the path of the built .so."""
+    os.makedirs(OBJ_DIR, exist_ok=True)
+    cc = hipcc()
+    inc = ["-I", os.path.join(ROOT, "include"), "-I", CSRC]
+    objs = [os.path.join(OBJ_DIR, os.path.splitext(s)[0] + ".o") for s in SOURCES]
+    cmds = [[cc, *HIPCC_FLAGS, *extra_flags, *inc, "-c", os.path.join(CSRC, s), "-o", o]
+            for s, o in zip(SOURCES, objs)]
+    jobs = jobs or max(1, min(len(cmds), os.cpu_count() or 1))
+    with ThreadPoolExecutor(max_workers=jobs) as pool:
+        for f in [pool.submit(_run, c, verbose) for c in cmds]:
+            f.result()
+    tmp = LIB + ".tmp"
+    _run([cc, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp], verbose)
     os.replace(tmp, LIB)
     return LIB
 
