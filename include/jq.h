@@ -48,8 +48,10 @@
  *   - Arguments are checked before anything is launched: on any error nothing
  *     is written.  A failed kernel launch returns JQ_ERR_HIP; faults during
  *     execution surface at the caller's next synchronisation.
- *   - There is no global mutable state: calls may be made from several host
- *     threads at once (on one stream they execute in issue order).
+ *   - There is no global mutable state apart from the device scratch of
+ *     jq_w4a4_f6_linear_noalloc (and the per-device address of it, resolved
+ *     once under a lock): calls may be made from several host threads at once
+ *     (on one stream they execute in issue order).
  */
 #ifndef JQ_H
 #define JQ_H
@@ -407,6 +409,36 @@ jq_status jq_w4a4_f6_linear(const void* x_bf16, int64_t M, int64_t K,
                             const void* wf6, const float* w_scale, int64_t N,
                             const void* bias_bf16, void* y_bf16,
                             void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Size of the device scratch that libjq holds for jq_w4a4_f6_linear_noalloc
+ * on each device it runs on (96 MiB): room for the BF6 activation operand and
+ * the scales of an input of up to about 128 M elements, e.g. the FLUX-12B
+ * MLP-down input of two images, 9216 x 12288 (81 MiB).
+ */
+#define JQ_NOALLOC_SCRATCH_BYTES ((size_t)96 << 20)
+
+/*
+ * jq_w4a4_f6_linear for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): the same layer, kernels and result, with the quantised
+ * activations (BF6 operand, then scales) in a scratch array the library
+ * holds on each device instead of a caller workspace.  The call allocates
+ * nothing and calls no allocating routine; its first call on a device looks
+ * up the scratch's address there.  The caller still passes inputs and
+ * outputs, with the meaning and layout of jq_w4a4_f6_linear.
+ * Nothing in the scratch needs to start at zero: every byte the GEMM reads
+ * (the whole operand, padding included, and M scales) is written by the
+ * call's own quantiser first.  All calls on one device share the one scratch
+ * and it keeps the last call's contents: calls that can overlap on one device
+ * (other streams, other host threads) race and must be ordered by the caller.
+ * Errors: as jq_w4a4_f6_linear; JQ_ERR_WORKSPACE_TOO_SMALL when
+ * jq_w4a4_f6_workspace_bytes(M,K) exceeds JQ_NOALLOC_SCRATCH_BYTES (checked
+ * before anything is launched).
+ */
+jq_status jq_w4a4_f6_linear_noalloc(const void* x_bf16, int64_t M, int64_t K,
+                                    const void* wf6, const float* w_scale, int64_t N,
+                                    const void* bias_bf16, void* y_bf16, void* stream);
 
 /*
  * GEMM + epilogue of the BF6 engine on an already-quantised activation

@@ -84,9 +84,11 @@
 #include <stdint.h>
 
 #include <algorithm>
+#include <mutex>
 #include <type_traits>
 
 #include "gemm_common.h"
+#include "jq.h"
 #include "jq_internal.h"
 
 namespace jq {
@@ -1429,6 +1431,37 @@ hipError_t launch_w4a4_f6_gemm(Epilogue epi, const uint8_t* xf6, const float* sx
 #undef JQ_F6_EPI
 #undef JQ_F6
   return hipGetLastError();
+}
+
+
+// ---------------------------------------------------------------------------
+// Library-held scratch of the allocation-free entry point
+// (jq_w4a4_f6_linear_noalloc): the BF6 activation operand and the scales of
+// one call, JQ_NOALLOC_SCRATCH_BYTES at most.  Each device the library runs
+// on holds its own copy until the process ends.  In host code the name is
+// only a handle for hipGetSymbolAddress; kernels get the device address it
+// returns, as they get a workspace.
+
+static __device__ __align__(256) uint8_t scratch[JQ_NOALLOC_SCRATCH_BYTES];
+
+hipError_t noalloc_scratch(void** ptr) {
+  constexpr int kMaxDevices = 64;
+  static std::mutex mu;
+  static void* addr[kMaxDevices] = {};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (addr[dev] == nullptr) {
+    // once per device, with that device current
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    addr[dev] = p;
+  }
+  *ptr = addr[dev];
+  return hipSuccess;
 }
 
 }  // namespace jq

@@ -321,6 +321,20 @@ size_t f6_workspace_bytes(int64_t M, int64_t K) {
          round_up(static_cast<size_t>(M) * sizeof(float), kWsAlign);
 }
 
+// Quantise x into a checked workspace (BF6 operand, then scales), then the
+// GEMM with the fused epilogue.
+jq_status f6_linear_launch(const void* x_bf16, int64_t M, int64_t K, const void* wf6, const float* w_scale,
+                           int64_t N, const void* bias_bf16, void* y_bf16, void* workspace, void* stream) {
+  uint8_t* xf6 = static_cast<uint8_t*>(workspace);
+  float* sx = reinterpret_cast<float*>(xf6 + round_up(static_cast<size_t>(jq::f6_operand_bytes(M, K)), kWsAlign));
+  hipError_t e = jq::launch_quantize_rows_f6(static_cast<const uint16_t*>(x_bf16), M, K, xf6, sx,
+                                             as_stream(stream));
+  if (e != hipSuccess) return JQ_ERR_HIP;
+  e = jq::launch_w4a4_f6_gemm(jq::Epilogue::kBf16, xf6, sx, M, K, static_cast<const uint8_t*>(wf6), w_scale, N,
+                              static_cast<const uint16_t*>(bias_bf16), y_bf16, as_stream(stream));
+  return from_hip(e);
+}
+
 jq_status check_group_f6_gemm(const void* xf6, const float* sx, int64_t M, int64_t K, int64_t G, const void* wf6,
                               const float* sw, int64_t N, const void* bias, const void* y) {
   if (xf6 == nullptr || wf6 == nullptr || y == nullptr || sx == nullptr || sw == nullptr) return JQ_ERR_INVALID_ARG;
@@ -400,14 +414,20 @@ jq_status jq_w4a4_f6_linear(const void* x_bf16, int64_t M, int64_t K, const void
   if (st != JQ_OK) return st;
   if (!aligned(workspace, kWsAlign)) return JQ_ERR_MISALIGNED;
   if (workspace_bytes < f6_workspace_bytes(M, K)) return JQ_ERR_WORKSPACE_TOO_SMALL;
-  uint8_t* xf6 = static_cast<uint8_t*>(workspace);
-  float* sx = reinterpret_cast<float*>(xf6 + round_up(static_cast<size_t>(jq::f6_operand_bytes(M, K)), kWsAlign));
-  hipError_t e = jq::launch_quantize_rows_f6(static_cast<const uint16_t*>(x_bf16), M, K, xf6, sx,
-                                             as_stream(stream));
-  if (e != hipSuccess) return JQ_ERR_HIP;
-  e = jq::launch_w4a4_f6_gemm(jq::Epilogue::kBf16, xf6, sx, M, K, static_cast<const uint8_t*>(wf6), w_scale, N,
-                              static_cast<const uint16_t*>(bias_bf16), y_bf16, as_stream(stream));
-  return from_hip(e);
+  return f6_linear_launch(x_bf16, M, K, wf6, w_scale, N, bias_bf16, y_bf16, workspace, stream);
+}
+
+jq_status jq_w4a4_f6_linear_noalloc(const void* x_bf16, int64_t M, int64_t K, const void* wf6,
+                                    const float* w_scale, int64_t N, const void* bias_bf16, void* y_bf16,
+                                    void* stream) {
+  if (x_bf16 == nullptr) return JQ_ERR_INVALID_ARG;
+  // the activation operand lives in the library's scratch; check the rest with stand-ins
+  const jq_status st = check_f6_gemm(x_bf16, w_scale, M, K, wf6, w_scale, N, bias_bf16, y_bf16, true);
+  if (st != JQ_OK) return st;
+  if (f6_workspace_bytes(M, K) > JQ_NOALLOC_SCRATCH_BYTES) return JQ_ERR_WORKSPACE_TOO_SMALL;
+  void* scratch = nullptr;
+  if (jq::noalloc_scratch(&scratch) != hipSuccess) return JQ_ERR_HIP;
+  return f6_linear_launch(x_bf16, M, K, wf6, w_scale, N, bias_bf16, y_bf16, scratch, stream);
 }
 
 jq_status jq_w4a4_f6_gemm(const void* xf6, const float* scale, int64_t M, int64_t K, const void* wf6,

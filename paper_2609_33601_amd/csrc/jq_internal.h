@@ -80,6 +80,10 @@ hipError_t launch_w4a4_f6_gemm(Epilogue epi, const uint8_t* xf6, const float* sx
                                const uint8_t* wf6, const float* sw, int64_t N, const uint16_t* bias, void* out,
                                hipStream_t st);
 
+// Device address of the library-held scratch (JQ_NOALLOC_SCRATCH_BYTES) on
+// the current device, resolved once per device.
+hipError_t noalloc_scratch(void** ptr);
+
 }  // namespace jq
 
 #endif  // JQ_INTERNAL_H

@@ -47,6 +47,7 @@ SIGNATURES = {
     "jq_ternary_to_f6_weight": (ctypes.c_int, [_vp, _i64, _i64, _vp, _vp]),
     "jq_w4a4_f6_workspace_bytes": (_sz, [_i64, _i64]),
     "jq_w4a4_f6_linear": (ctypes.c_int, [_vp, _i64, _i64, _vp, _fp, _i64, _vp, _vp, _vp, _sz, _vp]),
+    "jq_w4a4_f6_linear_noalloc": (ctypes.c_int, [_vp, _i64, _i64, _vp, _fp, _i64, _vp, _vp, _vp]),
     "jq_w4a4_f6_gemm": (ctypes.c_int, [_vp, _fp, _i64, _i64, _vp, _fp, _i64, _vp, _vp, _vp]),
     "jq_w4a4_f6_gemm_i32": (ctypes.c_int, [_vp, _i64, _i64, _vp, _i64, _ip, _vp]),
     "jq_f6_gemm_plan": (ctypes.c_int, [_i64, _i64, _i64, ctypes.c_int, _ip, _ip]),
@@ -452,6 +453,27 @@ def jq_w4a4_f6_linear(x, wf6, w_scale, bias=None, y=None, workspace=None, stream
                                  _dev(workspace, torch.uint8, None, "workspace"), workspace.numel(),
                                  _stream_ptr(stream))
     _check(st, "jq_w4a4_f6_linear")
+    return y
+
+
+# The library-held scratch of jq_w4a4_f6_linear_noalloc, per device (include/jq.h).
+JQ_NOALLOC_SCRATCH_BYTES = 96 << 20
+
+
+def jq_w4a4_f6_linear_noalloc(x, wf6, w_scale, bias=None, y=None, stream=None):
+    """jq_w4a4_f6_linear with its workspace in the library's own device scratch
+    (allocates nothing itself; calls that overlap on one device race); returns bf16 [M,N]."""
+    torch = _torch()
+    M, K = x.shape
+    N = w_scale.shape[0]
+    if y is None:
+        y = torch.empty((M, N), dtype=torch.bfloat16, device=x.device)
+    bptr = ctypes.c_void_p(None) if bias is None else _dev(bias, torch.bfloat16, (N,), "bias")
+    st = lib().jq_w4a4_f6_linear_noalloc(_dev(x, torch.bfloat16, None, "x"), M, K,
+                                         _dev(wf6, torch.uint8, (jq_f6_operand_bytes(N, K),), "wf6"),
+                                         _dev(w_scale, torch.float32, (N,), "w_scale"), N, bptr,
+                                         _dev(y, torch.bfloat16, (M, N), "y"), _stream_ptr(stream))
+    _check(st, "jq_w4a4_f6_linear_noalloc")
     return y
 
 

@@ -31,7 +31,7 @@ def header_functions():
 
 def test_exports_every_declared_symbol():
     names = header_functions()
-    assert len(names) == 33, names
+    assert len(names) == 34, names
     lib = ctypes.CDLL(jq.LIB_PATH)
     for n in names:
         assert hasattr(lib, n), f"libjq.so does not export {n}"
@@ -232,6 +232,26 @@ def test_f6_gemm_and_linear_validation():
     assert L.jq_w4a4_f6_gemm_i32(A, 8, 64, A, 8, MIS, None) == jq.JQ_ERR_MISALIGNED
     # operands of 2 GiB or more are refused (31-bit buffer descriptors)
     assert L.jq_w4a4_f6_gemm_i32(A, 1 << 22, 65536, A, 8, A, None) == jq.JQ_ERR_UNSUPPORTED_SHAPE
+
+
+def test_f6_linear_noalloc_validation():
+    # argument checks of the allocation-free linear, all before the scratch is looked up
+    L = jq.lib()
+    f = L.jq_w4a4_f6_linear_noalloc
+    assert f(None, 8, 64, A, A, 8, None, A, None) == jq.JQ_ERR_INVALID_ARG
+    assert f(A, 8, 64, None, A, 8, None, A, None) == jq.JQ_ERR_INVALID_ARG
+    assert f(A, 8, 64, A, None, 8, None, A, None) == jq.JQ_ERR_INVALID_ARG
+    assert f(A, 8, 64, A, A, 8, None, None, None) == jq.JQ_ERR_INVALID_ARG
+    assert f(A, 0, 64, A, A, 8, None, A, None) == jq.JQ_ERR_INVALID_ARG
+    assert f(A, 8, 96, A, A, 8, None, A, None) == jq.JQ_ERR_UNSUPPORTED_SHAPE
+    assert f(MIS, 8, 64, A, A, 8, None, A, None) == jq.JQ_ERR_MISALIGNED
+    assert f(A, 8, 64, A, A, 8, A + 1, A, None) == jq.JQ_ERR_MISALIGNED
+    # the largest input the scratch holds, and the first beyond it
+    assert jq.JQ_NOALLOC_SCRATCH_BYTES == 96 << 20
+    assert L.jq_w4a4_f6_workspace_bytes(9216, 12288) <= jq.JQ_NOALLOC_SCRATCH_BYTES
+    assert L.jq_w4a4_f6_workspace_bytes(9216, 16384) > jq.JQ_NOALLOC_SCRATCH_BYTES
+    assert f(A, 9216, 16384, A, A, 8, None, A, None) == jq.JQ_ERR_WORKSPACE_TOO_SMALL
+    assert f(A, 1 << 20, 128, A, A, 8, None, A, None) == jq.JQ_ERR_WORKSPACE_TOO_SMALL
 
 
 def test_group_f6_validation():
