@@ -200,10 +200,12 @@ def epilogue(acc, s_x, s_w, bias_bits=None):
     acc = np.asarray(acc)
     assert np.all(np.abs(acc) < 2 ** 24)
     t = acc.astype(np.float32)
-    t = (t * np.asarray(s_x, dtype=np.float32)[:, None]).astype(np.float32)
-    t = (t * np.asarray(s_w, dtype=np.float32)[None, :]).astype(np.float32)
-    if bias_bits is not None:
-        t = (t + bf16_bits_to_f32(bias_bits)[None, :]).astype(np.float32)
+    # rows near the bf16 maximum may overflow to +-inf, the IEEE result
+    with np.errstate(over="ignore", invalid="ignore"):
+        t = (t * np.asarray(s_x, dtype=np.float32)[:, None]).astype(np.float32)
+        t = (t * np.asarray(s_w, dtype=np.float32)[None, :]).astype(np.float32)
+        if bias_bits is not None:
+            t = (t + bf16_bits_to_f32(bias_bits)[None, :]).astype(np.float32)
     return f32_to_bf16_bits(t)
 
 
