@@ -5,8 +5,8 @@ Bars, as for the packed-int4 path: scales, codes and int32 accumulators
 bit-exact; bf16 outputs within 1 bf16 ulp of the oracle (expected
 bit-identical).  The codes inside a BF6 operand are read back with a decoder of
 the layout documented in include/jq.h, written here from that description.
-At full workload sizes the engine's outputs are also compared bit for bit with
-the packed-int4 engine's, and sampled rows with the oracle.
+At full workload sizes every output and accumulator is compared with the
+oracle in tests/test_gpu_full_oracle.py.
 """
 
 import os
@@ -332,33 +332,6 @@ def test_f6_gemm_matches_linear():
     assert torch.equal(y1.view(torch.int16), y2.view(torch.int16))
 
 
-def _sample_rows(M, n=24, seed=0):
-    rng = np.random.default_rng(seed)
-    rows = set(r for r in [0, 1, 255, 256, M // 2, M - 257, M - 1] if 0 <= r < M)
-    rows.update(rng.integers(0, M, size=n).tolist())
-    return np.array(sorted(rows))
-
-
-@pytest.mark.parametrize("lin", [l for wl in workloads.WORKLOADS.values() for l in wl.linears
-                                 if l.name != "tiny"], ids=lambda l: l.name)
-def test_f6_linear_full_size(lin):
-    """Full-size layer: bit-identical to the packed-int4 engine, sampled rows vs the oracle."""
-    say("f6 linear full", lin.name, lin.M, lin.K, lin.N)
-    x_bits, w_bits, b_bits = lin.make_x(), lin.make_w(), lin.make_bias()
-    x = dev_bf16(x_bits)
-    wq, sw = jq.jq_pack_weight_int4(dev_bf16(w_bits))
-    wf6 = jq.jq_int4_to_f6_weight(wq)
-    b = None if b_bits is None else dev_bf16(b_bits)
-    y6 = jq.jq_w4a4_f6_linear(x, wf6, sw, b)
-    y4 = jq.jq_w4a4_linear(x, wq, sw, b)
-    torch.cuda.synchronize()
-    diff = int((y6.view(torch.int16) != y4.view(torch.int16)).sum())
-    assert diff == 0, f"{diff} outputs differ from the packed-int4 engine"
-    rows = _sample_rows(lin.M, seed=lin.N)
-    ref = oracle.w4a4_linear_rows(x_bits, wq.cpu().numpy(), sw.cpu().numpy(), rows, b_bits)
-    assert_bf16_close(jq.bf16_bits(y6[torch.from_numpy(rows).cuda()]), ref, lin.name)
-
-
 # ---------------------------------------------------------------------------
 # W1.58A4 on the BF6 engine: ternary codes in the BF6 weight layout
 # ---------------------------------------------------------------------------
@@ -414,18 +387,3 @@ def test_f6_w158a4_linear_ragged(M, K, N, bias):
     y6, y8, wt, g = f6_ternary_layer(x, w, b)
     assert torch.equal(y6.view(torch.int16), y8.view(torch.int16))
     assert_bf16_close(jq.bf16_bits(y6), oracle.w158a4_linear(x, wt, g, b), f"f6 ternary {M}x{K}->{N}")
-
-
-@pytest.mark.parametrize("lin", [workloads.FLUX_MLP.linears[0], workloads.FLUX_MLP.linears[1],
-                                 workloads.WORKLOADS["dllm_block"].linears[0]], ids=lambda l: l.name)
-def test_f6_w158a4_linear_full_size(lin):
-    """Full-size W1.58A4 layer on the BF6 engine: bit-identical to the int8
-    engine's W1.58A4 layer, sampled rows vs the oracle."""
-    say("f6 ternary linear full", lin.name, lin.M, lin.K, lin.N)
-    x_bits, w_bits, b_bits = lin.make_x(), lin.make_w(), lin.make_bias()
-    y6, y8, wt, g = f6_ternary_layer(x_bits, w_bits, b_bits)
-    diff = int((y6.view(torch.int16) != y8.view(torch.int16)).sum())
-    assert diff == 0, f"{diff} outputs differ from the int8 engine's W1.58A4 layer"
-    rows = _sample_rows(lin.M, seed=lin.N + 1)
-    ref = oracle.w158a4_linear_rows(x_bits, wt, g, rows, b_bits)
-    assert_bf16_close(jq.bf16_bits(y6[torch.from_numpy(rows).cuda()]), ref, lin.name)

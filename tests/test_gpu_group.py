@@ -4,7 +4,9 @@ Bars: packed codes and fp32 group scales bit-exact; the fp32 group sum S
 (exposed by jq_w4a4g_gemm_f32) bit-exact, since both sides add the same
 rounded terms in the same order; bf16 outputs within 1 bf16 ulp (expected
 bit-identical).  Full-size layers are checked on whole quantised tensors and on
-sampled output rows.
+sampled output rows: the oracle's group product keeps every group's exact
+partial sum ([M, N, K/G] integers), which at full size would take tens of GB
+and minutes per layer, so only rows are drawn from it there.
 """
 
 import numpy as np

@@ -3,8 +3,8 @@
 Bars: packed int4 codes, fp32 scales and int32 accumulators bit-exact; bf16
 outputs within 1 bf16 ulp of the oracle (and in fact expected bit-identical,
 since the kernel follows the same rounding sequence).  Full-size workloads are
-checked on whole quantised tensors and on sampled output rows, which the oracle
-computes row by row.
+checked here on whole quantised tensors; every output and accumulator of the
+full-size layers is compared with the oracle in tests/test_gpu_full_oracle.py.
 """
 
 import os
@@ -287,35 +287,6 @@ def _sample_rows(M, n=40, seed=0):
     rows = set(r for r in fixed if 0 <= r < M)
     rows.update(rng.integers(0, M, size=n).tolist())
     return np.array(sorted(rows))
-
-
-@pytest.mark.parametrize("lin", [l for wl in workloads.WORKLOADS.values() for l in wl.linears
-                                 if l.name != "tiny"], ids=lambda l: l.name)
-def test_linear_full_size_sampled(lin):
-    """Full-size layer exactly as the benchmark launches it; sampled rows vs the oracle."""
-    say("linear full", lin.name, lin.M, lin.K, lin.N)
-    x_bits, w_bits, b_bits = lin.make_x(), lin.make_w(), lin.make_bias()
-    x = dev_bf16(x_bits)
-    wq, sw = jq.jq_pack_weight_int4(dev_bf16(w_bits))
-    b = None if b_bits is None else dev_bf16(b_bits)
-    ws = torch.empty(jq.jq_w4a4_workspace_bytes(lin.M, lin.K), dtype=torch.uint8, device="cuda")
-    y = jq.jq_w4a4_linear(x, wq, sw, b, workspace=ws)
-    qx_dev = ws[: lin.M * lin.K // 2].view(lin.M, lin.K // 2)
-    acc = jq.jq_w4a4_gemm_i32(qx_dev, wq)
-    torch.cuda.synchronize()
-    rows = _sample_rows(lin.M, seed=lin.N)
-    wq_h, sw_h = wq.cpu().numpy(), sw.cpu().numpy()
-    rq, rs = oracle.pack_weight_int4(w_bits)
-    assert np.array_equal(wq_h, rq) and np.array_equal(sw_h.view(np.uint32), rs.view(np.uint32))
-    qx_h = qx_dev[torch.from_numpy(rows).cuda()].cpu().numpy()
-    rqx, rsx = oracle.quantize_act(x_bits[rows])
-    assert np.array_equal(qx_h, rqx), "workspace codes differ"
-    ref_acc = oracle.w4a4_gemm_i32(rqx, rq)
-    got_acc = acc[torch.from_numpy(rows).cuda()].cpu().numpy()
-    assert np.array_equal(got_acc, ref_acc), "accumulators differ"
-    y_rows = jq.bf16_bits(y[torch.from_numpy(rows).cuda()])
-    ref = oracle.epilogue(ref_acc, rsx, rs, b_bits)
-    assert_bf16_close(y_rows, ref, lin.name)
 
 
 def test_shared_quantization_matches_linear():
