@@ -411,6 +411,31 @@ jq_status jq_w4a4_f6_linear(const void* x_bf16, int64_t M, int64_t K,
                             void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * The per-token quantiser of jq_quantize_act_f6 on several independent
+ * inputs at once (at most JQ_QUANT_BATCH_MAX): input i, x_bf16[i] [M[i], K[i]]
+ * bf16, is quantised into xf6[i] (jq_f6_operand_bytes(M[i], K[i]) bytes, the
+ * activation layout) and scale[i] [M[i]] fp32, exactly as jq_quantize_act_f6
+ * would.  Inputs of up to 16384 codes per row share one launch, so the short
+ * quantisation of one input runs inside the bandwidth-bound pass over
+ * another instead of as a launch of its own, e.g. the inputs of two linears
+ * that do not depend on each other; longer rows get a launch each, on the
+ * same stream.  The quantisation and packing kernels are part of the
+ * deployed low-bit operator (appendix FAQ Q7); the paper names the
+ * non-GEMM time of a step as what makes speed-ups hard to reach on small
+ * models (deployment-summary figure caption, Sec. 1).
+ *   count   1 .. JQ_QUANT_BATCH_MAX
+ *   x_bf16, M, K, xf6, scale   host arrays of count entries; every entry
+ *           obeys jq_quantize_act_f6's rules; no output may overlap another
+ *           entry's input or output
+ * Errors: JQ_ERR_INVALID_ARG (count out of range, a NULL array or entry,
+ * non-positive sizes), JQ_ERR_UNSUPPORTED_SHAPE, JQ_ERR_MISALIGNED, JQ_ERR_HIP;
+ * every entry is checked before anything is launched.
+ */
+#define JQ_QUANT_BATCH_MAX 8
+jq_status jq_quantize_act_f6_batch(int count, const void* const* x_bf16, const int64_t* M, const int64_t* K,
+                                   void* const* xf6, float* const* scale, void* stream);
+
+/*
  * Size of the device scratch that libjq holds for jq_w4a4_f6_linear_noalloc
  * on each device it runs on (96 MiB): room for the BF6 activation operand and
  * the scales of an input of up to about 128 M elements, e.g. the FLUX-12B

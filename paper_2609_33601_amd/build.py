@@ -18,6 +18,10 @@ LIB = os.path.join(PKG, "libjq.so")
 SOURCES = ["quantize.hip", "ternary.hip", "gemm.hip", "gemm_group.hip", "f6.hip", "jq_api.cpp"]
 ARCH = "gfx950"
 
+# Per-source flags: the BF6 kernels are built without machine sinking, which
+# would move the first k-step's MFMAs of a GEMM stage below its barrier.
+SOURCE_FLAGS = {"f6.hip": ["-mllvm", "-disable-machine-sink"]}
+
 HIPCC_FLAGS = [
     f"--offload-arch={ARCH}",
     "-O3",
@@ -55,7 +59,7 @@ def build(verbose=False, extra_flags=(), jobs=None):
     cc = hipcc()
     inc = ["-I", os.path.join(ROOT, "include"), "-I", CSRC]
     objs = [os.path.join(OBJ_DIR, os.path.splitext(s)[0] + ".o") for s in SOURCES]
-    cmds = [[cc, *HIPCC_FLAGS, *extra_flags, *inc, "-c", os.path.join(CSRC, s), "-o", o]
+    cmds = [[cc, *HIPCC_FLAGS, *SOURCE_FLAGS.get(s, []), *extra_flags, *inc, "-c", os.path.join(CSRC, s), "-o", o]
             for s, o in zip(SOURCES, objs)]
     jobs = jobs or max(1, min(len(cmds), os.cpu_count() or 1))
     with ThreadPoolExecutor(max_workers=jobs) as pool:

@@ -75,6 +75,23 @@
 //     the DMA three stages ahead into the slot just read; then the MFMAs of
 //     k-step 1 run while the next stage's k-step 0 fragments are read.  No
 //     VALU work sits between the MFMAs.
+//   * Every vector-memory instruction of the stage loop (the weight loads
+//     and the buffer -> LDS transfers) is issued as an instruction of its
+//     own, and the loop orders it with explicit waits only: at a stage's
+//     start, after issuing the next stage's weights, vmcnt(9) (this stage's
+//     weights have landed); at its middle, vmcnt(9), lgkmcnt(0) and the
+//     barrier (the next slot's DMA has landed and every read of the slot
+//     about to be refilled has completed).  Left to the compiler, the
+//     transfers made it wait for every DMA in flight before each LDS read.
+//     The file is also built without machine sinking, which otherwise moved
+//     the first k-step's MFMAs below the stage's barrier (into the block
+//     after the tile's first-stage branch), leaving the matrix pipes idle
+//     while both waves of a SIMD waited there.
+//   * Operands reach the MFMAs without register copies: a band's three
+//     weight loads of a stage fill 12 consecutive registers, whose first
+//     and last six are the two k-steps' operands, and an activation
+//     fragment's 16- and 8-byte parts land next to each other (the 8-byte
+//     part read on its own, not paired with another fragment's).
 //   * The weight fragment is operand A and the activation fragment operand B,
 //     so the 32x32 result is y^T: lane L holds column m = L % 32 and rows
 //     n = 8j + 4(L / 32) + r (j, r = 0..3).  The epilogue scales them, packs
@@ -108,6 +125,7 @@ constexpr int kFragBytes = 1536;          // one 32-row x 64-code fragment
 constexpr int kFBN = 256;                 // block tile columns
 constexpr int kDmaPerWave = 3;            // stage DMA instructions per wave
 constexpr int64_t kShortK = 6144;          // largest K that may take the two-block shape
+constexpr int kQuantBatchMax = 8;          // inputs of one batched quantiser launch
 
 // The GEMM comes in two block shapes (WAVES = 8 or 4 waves of 64): one
 // 8-wave block per CU on a tile of up to 256 activation rows, or two 4-wave
@@ -361,14 +379,18 @@ __device__ __forceinline__ int64_t row0_of_block4(int64_t b) {
 // maxima meet by shuffles within a wave and through LDS across waves; group
 // maxima (G = 64, 128) by shuffles between the lanes of a group.  The scales
 // and codes are those of quantize_rows_f6_kernel.
+//
+// The body is shared with the batched form (several inputs in one launch):
+// block b of the input, and nj <= NJ sets of groups per wave (the rest of the
+// register arrays idle).
 template <int NJ, int G>
-__global__ __launch_bounds__(512) void quantize_rows4_f6_kernel(const uint16_t* __restrict__ x, int64_t M, int64_t K,
-                                                                int64_t rows_padded, int64_t ksteps,
-                                                                uint8_t* __restrict__ out, float* __restrict__ scale) {
+__device__ __forceinline__ void q4_rows(const uint16_t* __restrict__ x, int64_t M, int64_t K, int64_t rows_padded,
+                                        int64_t ksteps, uint8_t* __restrict__ out, float* __restrict__ scale,
+                                        int64_t b, int nj) {
   __shared__ uint32_t wave_max[8][4];
   const int T = blockDim.x;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nwaves = T >> 6;
-  const int64_t row0 = row0_of_block4(blockIdx.x);
+  const int64_t row0 = row0_of_block4(b);
   if (row0 >= rows_padded) return;
   const int rr = lane & 3, gslot = lane >> 2;
   const int64_t row = row0 + rr;
@@ -382,6 +404,7 @@ __global__ __launch_bounds__(512) void quantize_rows4_f6_kernel(const uint16_t* 
   v4u32 t[NJ][4];
 #pragma unroll
   for (int j = 0; j < NJ; ++j) {
+    if (j >= nj) break;
     const int g0 = 16 * (nwaves * j + wave);
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
@@ -396,6 +419,7 @@ __global__ __launch_bounds__(512) void quantize_rows4_f6_kernel(const uint16_t* 
   uint4 v[NJ][4];
 #pragma unroll
   for (int j = 0; j < NJ; ++j) {
+    if (j >= nj) break;
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
@@ -413,7 +437,10 @@ __global__ __launch_bounds__(512) void quantize_rows4_f6_kernel(const uint16_t* 
   // The lane's maximum over each of its groups.
   uint32_t gmax[NJ];
 #pragma unroll
+  for (int j = 0; j < NJ; ++j) gmax[j] = 0;  // sets past nj stay 0
+#pragma unroll
   for (int j = 0; j < NJ; ++j) {
+    if (j >= nj) break;
     u16x2 gm = {0, 0};
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
@@ -447,6 +474,7 @@ __global__ __launch_bounds__(512) void quantize_rows4_f6_kernel(const uint16_t* 
   }
 #pragma unroll
   for (int j = 0; j < NJ; ++j) {
+    if (j >= nj) break;
     float s = srow;
     if constexpr (G != 0) {
       constexpr int kLanes = G / 32;  // group slots per group, 4 lanes apart
@@ -477,6 +505,38 @@ __global__ __launch_bounds__(512) void quantize_rows4_f6_kernel(const uint16_t* 
     }
     store_group<false>(out, ksteps, row, gi, bf6_group(q));
   }
+}
+
+template <int NJ, int G>
+__global__ __launch_bounds__(512) void quantize_rows4_f6_kernel(const uint16_t* __restrict__ x, int64_t M, int64_t K,
+                                                                int64_t rows_padded, int64_t ksteps,
+                                                                uint8_t* __restrict__ out, float* __restrict__ scale) {
+  q4_rows<NJ, G>(x, M, K, rows_padded, ksteps, out, scale, blockIdx.x, NJ);
+}
+
+// Several independent inputs quantised per token in one launch (rows of up
+// to 512 groups each): input i takes the blocks from first[i] on, a multiple
+// of 64 so that each band's blocks stay on one XCD, and runs with nj[i] of
+// the NJ sets of groups per wave.  Each input's codes and scales are those
+// of its own launch of quantize_rows4_f6_kernel.
+struct Q4Input {
+  const uint16_t* x;
+  uint8_t* out;
+  float* scale;
+  int64_t M, K, rows_padded, ksteps, first;
+  int nj;
+};
+struct Q4Batch {
+  Q4Input in[kQuantBatchMax];
+  int count;
+};
+
+template <int NJ>
+__global__ __launch_bounds__(512) void quantize_rows4_f6_batch_kernel(Q4Batch b) {
+  int i = 0;
+  while (i + 1 < b.count && static_cast<int64_t>(blockIdx.x) >= b.in[i + 1].first) ++i;
+  const Q4Input& e = b.in[i];
+  q4_rows<NJ, 0>(e.x, e.M, e.K, e.rows_padded, e.ksteps, e.out, e.scale, blockIdx.x - e.first, e.nj);
 }
 
 // Canonical packed int4 codes (TERNARY false) or packed ternary codes (true)
@@ -526,8 +586,48 @@ typedef int v2i32 __attribute__((ext_vector_type(2)));
 struct WFrag {
   v8i f[2][2];  // [k-step][band]; dwords 0..5 used
 };
+// A wave's weights of one stage as loaded: three 16-byte parts per band
+// (the six dwords of k-step 0, then those of k-step 1), turned into MFMA
+// operands only once the stage's wait has passed.
+typedef int v12i __attribute__((ext_vector_type(12)));
+struct WRaw {
+  v12i p[2];  // [band]: the three parts in load order
+};
 
 __device__ __forceinline__ v8i join(v4i32 a, v2i32 b) { return v8i{a.x, a.y, a.z, a.w, b.x, b.y, 0, 0}; }
+
+// Buffer -> LDS transfers issued as instructions of their own (M0 set
+// alongside), so that the compiler neither tracks them nor orders LDS reads
+// behind them: the GEMM orders them against its LDS reads with its own
+// explicit waits, and is the only user of M0 in its kernel.
+typedef unsigned v4u32r __attribute__((ext_vector_type(4)));
+struct RawRsrc {
+  v4u32r w;  // the four descriptor words of a raw (unswizzled, stride 0) buffer
+};
+__device__ __forceinline__ RawRsrc raw_rsrc(const void* base, uint32_t bytes) {
+  const uint64_t a = reinterpret_cast<uint64_t>(base);
+  RawRsrc r;
+  r.w = v4u32r{static_cast<uint32_t>(a), static_cast<uint32_t>(a >> 32) & 0xFFFFu, bytes,
+               static_cast<uint32_t>(kBufferFlags)};
+  return r;
+}
+// The LDS byte address of a __shared__ object: the low 32 bits of its generic address.
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return static_cast<uint32_t>(reinterpret_cast<uintptr_t>(p));
+}
+__device__ __forceinline__ void dma16_raw(const RawRsrc& r, uint32_t lds, uint32_t voffset, uint32_t soffset) {
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
+               :: "s"(__builtin_amdgcn_readfirstlane(lds)), "v"(voffset), "s"(r.w), "s"(soffset) : "memory");
+}
+__device__ __forceinline__ v4i32 load16_raw(const RawRsrc& r, uint32_t voffset, uint32_t soffset) {
+  v4i32 v;
+  asm volatile("buffer_load_dwordx4 %0, %1, %2, %3 offen" : "=v"(v) : "v"(voffset), "s"(r.w), "s"(soffset));
+  return v;
+}
+__device__ __forceinline__ void dma4_raw(const RawRsrc& r, uint32_t lds, uint32_t voffset) {
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dword %1, %2, 0 offen lds"
+               :: "s"(__builtin_amdgcn_readfirstlane(lds)), "v"(voffset), "s"(r.w) : "memory");
+}
 
 constexpr int kWaitcntBase = (0x7 << 4) | (0xF << 8);  // expcnt, lgkmcnt: no wait
 constexpr int vmcnt_imm(int n) { return kWaitcntBase | (n & 0xF) | ((n >> 4) << 14); }
@@ -595,12 +695,8 @@ __global__ __launch_bounds__(64 * WAVES, 8 / WAVES) void w4a4_f6_gemm_kernel(
     *n0 = tc.tn * kFBN;
   };
 
-  const __amdgpu_buffer_rsrc_t rsx = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<uint8_t*>(xf6), 0, static_cast<int>(static_cast<int64_t>(mbands) * ksteps * kFragBytes),
-      kBufferFlags);
-  const __amdgpu_buffer_rsrc_t rsw = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<uint8_t*>(wf6), 0, static_cast<int>(static_cast<int64_t>(nbands) * ksteps * kFragBytes),
-      kBufferFlags);
+  const RawRsrc rsx = raw_rsrc(xf6, static_cast<uint32_t>(static_cast<int64_t>(mbands) * ksteps * kFragBytes));
+  const RawRsrc rsw = raw_rsrc(wf6, static_cast<uint32_t>(static_cast<int64_t>(nbands) * ksteps * kFragBytes));
 
   // Activation DMA: the 16 fragments of a stage ((k-step s, band b) in order
   // 8s + b) are contiguous 1536-byte blocks in LDS; slot part
@@ -634,23 +730,31 @@ __global__ __launch_bounds__(64 * WAVES, 8 / WAVES) void w4a4_f6_gemm_kernel(
 #pragma unroll
     for (int j = 0; j < kDmaPerWave; ++j) {
       const uint32_t band = static_cast<uint32_t>(min(m0 / 32 + rband[j], mbands - 1));
-      dma16(rsx, dst + 64 * j, rpart[j] == kOutside ? kOutside : band * band_bytes + rpart[j],
-            2 * kFragBytes * rot(st));
+      dma16_raw(rsx, lds_addr(dst + 64 * j), rpart[j] == kOutside ? kOutside : band * band_bytes + rpart[j],
+                2 * kFragBytes * rot(st));
     }
   };
-  auto load_w = [&](WFrag& w, int n0, int st) __attribute__((always_inline)) {
+  auto load_w = [&](WRaw& w, int n0, int st) __attribute__((always_inline)) {
 #pragma unroll
     for (int f = 0; f < 2; ++f) {
       const uint32_t wb = static_cast<uint32_t>(min(n0 / 32 + 2 * wn + f, nbands - 1)) * band_bytes;
-      const int so = 2 * rot(st) * kFragBytes;
-      const v4i32 p0 = __builtin_bit_cast(v4i32, __builtin_amdgcn_raw_buffer_load_b128(rsw, wb + 16 * lane, so, 0));
-      const v4i32 p1 =
-          __builtin_bit_cast(v4i32, __builtin_amdgcn_raw_buffer_load_b128(rsw, wb + 1024 + 16 * lane, so, 0));
-      const v4i32 p2 =
-          __builtin_bit_cast(v4i32, __builtin_amdgcn_raw_buffer_load_b128(rsw, wb + 2048 + 16 * lane, so, 0));
-      w.f[0][f] = v8i{p0.x, p0.y, p0.z, p0.w, p1.x, p1.y, 0, 0};
-      w.f[1][f] = v8i{p1.z, p1.w, p2.x, p2.y, p2.z, p2.w, 0, 0};
+      const uint32_t so = static_cast<uint32_t>(2 * rot(st) * kFragBytes);
+      const v4i32 p0 = load16_raw(rsw, wb + 16 * lane, so);
+      const v4i32 p1 = load16_raw(rsw, wb + 1024 + 16 * lane, so);
+      const v4i32 p2 = load16_raw(rsw, wb + 2048 + 16 * lane, so);
+      w.p[f] = v12i{p0.x, p0.y, p0.z, p0.w, p1.x, p1.y, p1.z, p1.w, p2.x, p2.y, p2.z, p2.w};
     }
+  };
+  // the MFMA operands of a loaded stage (after the wait for its loads)
+  auto frags = [&](const WRaw& w) __attribute__((always_inline)) {
+    WFrag r;
+#pragma unroll
+    for (int f = 0; f < 2; ++f) {
+      // the k-steps are the 6-dword windows of the 12 loaded dwords
+      r.f[0][f] = __builtin_shufflevector(w.p[f], w.p[f], 0, 1, 2, 3, 4, 5, -1, -1);
+      r.f[1][f] = __builtin_shufflevector(w.p[f], w.p[f], 6, 7, 8, 9, 10, 11, -1, -1);
+    }
+    return r;
   };
   // Scales and bias of the tile at (m0, n0) into LDS: waves 0..3 take a
   // quarter of s_x each, waves 4..7 a quarter of s_w, waves 0..1 half of the
@@ -660,34 +764,28 @@ __global__ __launch_bounds__(64 * WAVES, 8 / WAVES) void w4a4_f6_gemm_kernel(
       // every wave a quarter of s_w; waves 0, 1 half of s_x each, waves 2, 3
       // half of the bias each
       {
-        const __amdgpu_buffer_rsrc_t r =
-            __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(sw), 0, 4 * N, kBufferFlags);
-        dma4(r, sc_w + 64 * wave, 4 * static_cast<uint32_t>(n0 + 64 * wave + lane), 0);
+        const RawRsrc r = raw_rsrc(sw, 4 * N);
+        dma4_raw(r, lds_addr(sc_w + 64 * wave), 4 * static_cast<uint32_t>(n0 + 64 * wave + lane));
       }
       if (wave < 2) {
-        const __amdgpu_buffer_rsrc_t r =
-            __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(sx), 0, 4 * M, kBufferFlags);
-        dma4(r, sc_x + 64 * wave, 4 * static_cast<uint32_t>(m0 + 64 * wave + lane), 0);
+        const RawRsrc r = raw_rsrc(sx, 4 * M);
+        dma4_raw(r, lds_addr(sc_x + 64 * wave), 4 * static_cast<uint32_t>(m0 + 64 * wave + lane));
       } else if (HAS_BIAS) {
-        const __amdgpu_buffer_rsrc_t r =
-            __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(bias), 0, 2 * N, kBufferFlags);
-        dma4(r, sc_b + 64 * (wave - 2), 2 * static_cast<uint32_t>(n0 + 128 * (wave - 2) + 2 * lane), 0);
+        const RawRsrc r = raw_rsrc(bias, 2 * N);
+        dma4_raw(r, lds_addr(sc_b + 64 * (wave - 2)), 2 * static_cast<uint32_t>(n0 + 128 * (wave - 2) + 2 * lane));
       }
     } else if constexpr (EPI == Epilogue::kBf16) {
       const int q = wave & 3;
       if (wave < 4) {
-        const __amdgpu_buffer_rsrc_t r =
-            __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(sx), 0, 4 * M, kBufferFlags);
-        dma4(r, sc_x + 64 * q, 4 * static_cast<uint32_t>(m0 + 64 * q + lane), 0);
+        const RawRsrc r = raw_rsrc(sx, 4 * M);
+        dma4_raw(r, lds_addr(sc_x + 64 * q), 4 * static_cast<uint32_t>(m0 + 64 * q + lane));
       } else {
-        const __amdgpu_buffer_rsrc_t r =
-            __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(sw), 0, 4 * N, kBufferFlags);
-        dma4(r, sc_w + 64 * q, 4 * static_cast<uint32_t>(n0 + 64 * q + lane), 0);
+        const RawRsrc r = raw_rsrc(sw, 4 * N);
+        dma4_raw(r, lds_addr(sc_w + 64 * q), 4 * static_cast<uint32_t>(n0 + 64 * q + lane));
       }
       if (HAS_BIAS && wave < 2) {
-        const __amdgpu_buffer_rsrc_t r =
-            __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(bias), 0, 2 * N, kBufferFlags);
-        dma4(r, sc_b + 64 * wave, 2 * static_cast<uint32_t>(n0 + 128 * wave + 2 * lane), 0);
+        const RawRsrc r = raw_rsrc(bias, 2 * N);
+        dma4_raw(r, lds_addr(sc_b + 64 * wave), 2 * static_cast<uint32_t>(n0 + 128 * wave + 2 * lane));
       }
     }
   };
@@ -695,8 +793,12 @@ __global__ __launch_bounds__(64 * WAVES, 8 / WAVES) void w4a4_f6_gemm_kernel(
   // the 8-byte part.
   auto read_b = [&](int k, int s, int fm) __attribute__((always_inline)) {
     const uint8_t* p = reinterpret_cast<const uint8_t*>(slot(k)) + (s * S::kBands + 4 * wm + fm) * kFragBytes;
-    return join(*reinterpret_cast<const v4i32*>(p + 16 * lane),
-                *reinterpret_cast<const v2i32*>(p + 1024 + 8 * lane));
+    // the 8-byte part as a relaxed atomic load, which the compiler does not
+    // pair with another fragment's (a paired read lands both parts apart from
+    // their 16-byte parts and costs moves to join them)
+    const uint64_t hi = __hip_atomic_load(reinterpret_cast<const uint64_t*>(p + 1024 + 8 * lane), __ATOMIC_RELAXED,
+                                          __HIP_MEMORY_SCOPE_WAVEFRONT);
+    return join(*reinterpret_cast<const v4i32*>(p + 16 * lane), __builtin_bit_cast(v2i32, hi));
   };
 
   // The rest of the kernel, for a wave with NFM activation bands (four in
@@ -731,7 +833,7 @@ __global__ __launch_bounds__(64 * WAVES, 8 / WAVES) void w4a4_f6_gemm_kernel(
     }
   };
 
-  WFrag w0, w1;
+  WRaw w0, w1;
   {
     int m0, n0, st;
     load_w(w0, cn0, 0);
@@ -888,17 +990,24 @@ __global__ __launch_bounds__(64 * WAVES, 8 / WAVES) void w4a4_f6_gemm_kernel(
   // so DMA(g + 1), issued before those, has landed (the stores of an
   // epilogue in between only add to the count).  After a tile's last stage
   // comes its epilogue.
-  WFrag* wset[2] = {&w0, &w1};
+  WRaw* wset[2] = {&w0, &w1};
   int t = 0, ti = 0;
   auto stage = [&](auto I) __attribute__((always_inline)) {
     constexpr int i = decltype(I)::value;
     constexpr int cur = i % 3, nxt = (i + 1) % 3;
-    const WFrag& wc = *wset[i % 2];
     {
       int m0, n0, st;
       ahead(t, ti, 1, &m0, &n0, &st);
       load_w(*wset[(i + 1) % 2], n0, st);
     }
+    // This stage's weights (loaded at the previous stage) have landed once at
+    // most the loads issued since are in flight: the DMA issued at the
+    // previous stage's barrier and the weights just issued (vector loads
+    // complete in order).  The same wait covers the DMA issued one barrier
+    // earlier still (it is older).
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(kWLoads + kDmaPerWave));
+    __builtin_amdgcn_sched_barrier(0);
+    const WFrag wc = frags(*wset[i % 2]);
 #define JQ_F6_STEP(S, FM, BQ, NK, NS, NFM)                                                              \
   if constexpr (FM < nfm) {                                                                             \
     acc[0][FM] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(wc.f[S][0], BQ, acc[0][FM], 3, 3, 0, 127, \
@@ -1340,6 +1449,53 @@ hipError_t launch_quantize_f6(const uint16_t* x, int64_t M, int64_t K, uint8_t* 
 hipError_t launch_quantize_rows_f6(const uint16_t* x, int64_t M, int64_t K, uint8_t* out, float* scale,
                                    hipStream_t st) {
   return launch_quantize_f6<0>(x, M, K, out, scale, st);
+}
+
+hipError_t launch_quantize_rows_f6_batch(int count, const uint16_t* const* x, const int64_t* M, const int64_t* K,
+                                         uint8_t* const* out, float* const* scale, hipStream_t st) {
+  // Inputs whose rows fit the four-rows-per-block kernel (at most 512 groups)
+  // share one launch: its waves are the most any of them needs, and NJ the
+  // most sets of groups any of them needs at that wave count.  Longer rows get
+  // a launch of their own, on the same stream.
+  Q4Batch b{};
+  int waves = 1;
+  for (int i = 0; i < count; ++i) {
+    const int64_t groups = 2 * f6_ksteps(K[i]);
+    if (groups <= 512) waves = static_cast<int>(std::max<int64_t>(waves, std::min<int64_t>(8, (groups + 15) / 16)));
+  }
+  int NJ = 1;
+  int64_t first = 0;
+  for (int i = 0; i < count; ++i) {
+    const int64_t ksteps = f6_ksteps(K[i]);
+    const int64_t groups = 2 * ksteps;
+    if (groups > 512) {
+      const hipError_t e = launch_quantize_f6<0>(x[i], M[i], K[i], out[i], scale[i], st);
+      if (e != hipSuccess) return e;
+      continue;
+    }
+    Q4Input& q = b.in[b.count++];
+    q.x = x[i];
+    q.out = out[i];
+    q.scale = scale[i];
+    q.M = M[i];
+    q.K = K[i];
+    q.rows_padded = (M[i] + 31) / 32 * 32;
+    q.ksteps = ksteps;
+    q.first = first;
+    q.nj = static_cast<int>((groups + 16 * waves - 1) / (16 * waves));
+    NJ = std::max(NJ, q.nj);
+    first += (q.rows_padded / 32 + kNumXcd - 1) / kNumXcd * 8 * kNumXcd;  // as launch_q4f6's grid
+  }
+  if (b.count == 0) return hipSuccess;
+  const dim3 grid(static_cast<unsigned>(first));
+  const size_t lds = static_cast<size_t>(waves) * 256 * 16;
+#define JQ_Q4B(NN) hipLaunchKernelGGL((quantize_rows4_f6_batch_kernel<NN>), grid, dim3(64 * waves), lds, st, b)
+  if (NJ <= 1) JQ_Q4B(1);
+  else if (NJ <= 2) JQ_Q4B(2);
+  else if (NJ <= 3) JQ_Q4B(3);
+  else JQ_Q4B(4);
+#undef JQ_Q4B
+  return hipGetLastError();
 }
 
 hipError_t launch_quantize_groups_f6(const uint16_t* x, int64_t M, int64_t K, int G, uint8_t* out, float* scale,

@@ -376,6 +376,26 @@ jq_status jq_quantize_act_f6(const void* x_bf16, int64_t M, int64_t K, void* xf6
                                               static_cast<uint8_t*>(xf6), scale, as_stream(stream)));
 }
 
+jq_status jq_quantize_act_f6_batch(int count, const void* const* x_bf16, const int64_t* M, const int64_t* K,
+                                   void* const* xf6, float* const* scale, void* stream) {
+  if (count < 1 || count > JQ_QUANT_BATCH_MAX) return JQ_ERR_INVALID_ARG;
+  if (x_bf16 == nullptr || M == nullptr || K == nullptr || xf6 == nullptr || scale == nullptr)
+    return JQ_ERR_INVALID_ARG;
+  for (int i = 0; i < count; ++i) {
+    if (x_bf16[i] == nullptr || xf6[i] == nullptr || scale[i] == nullptr) return JQ_ERR_INVALID_ARG;
+    const jq_status st = check_shape(M[i], K[i]);
+    if (st != JQ_OK) return st;
+    if (!aligned(x_bf16[i], 16) || !aligned(xf6[i], 16) || !aligned(scale[i], 4)) return JQ_ERR_MISALIGNED;
+  }
+  const uint16_t* xs[JQ_QUANT_BATCH_MAX];
+  uint8_t* outs[JQ_QUANT_BATCH_MAX];
+  for (int i = 0; i < count; ++i) {
+    xs[i] = static_cast<const uint16_t*>(x_bf16[i]);
+    outs[i] = static_cast<uint8_t*>(xf6[i]);
+  }
+  return from_hip(jq::launch_quantize_rows_f6_batch(count, xs, M, K, outs, scale, as_stream(stream)));
+}
+
 jq_status jq_int4_to_f6(const void* q_packed, int64_t rows, int64_t K, void* f6, void* stream) {
   if (q_packed == nullptr || f6 == nullptr) return JQ_ERR_INVALID_ARG;
   const jq_status st = check_shape(rows, K);

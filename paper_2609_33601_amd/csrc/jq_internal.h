@@ -59,6 +59,11 @@ int f6_tile_bands(int64_t M, int64_t N, int64_t slots);
 hipError_t launch_quantize_rows_f6(const uint16_t* x, int64_t M, int64_t K, uint8_t* out, float* scale,
                                    hipStream_t st);
 
+// The per-token BF6 quantiser on `count` (<= 8) independent inputs at once
+// (one launch for those with K <= 16384, one each for longer rows).
+hipError_t launch_quantize_rows_f6_batch(int count, const uint16_t* const* x, const int64_t* M, const int64_t* K,
+                                         uint8_t* const* out, float* const* scale, hipStream_t st);
+
 // Group-wise BF6 engine (G = 64 or 128): the group quantiser writing the BF6
 // activation operand and scales [M, K/G]; the group GEMM on BF6 operands with
 // scales [M, K/G] and [N, K/G] (epi kBf16 or kF32).

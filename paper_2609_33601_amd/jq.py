@@ -42,6 +42,7 @@ SIGNATURES = {
     "jq_w4a4g_gemm_f32": (ctypes.c_int, [_vp, _fp, _i64, _i64, _i64, _vp, _fp, _i64, _fp, _vp]),
     "jq_f6_operand_bytes": (_sz, [_i64, _i64]),
     "jq_quantize_act_f6": (ctypes.c_int, [_vp, _i64, _i64, _vp, _fp, _vp]),
+    "jq_quantize_act_f6_batch": (ctypes.c_int, [ctypes.c_int, _vp, _vp, _vp, _vp, _vp, _vp]),
     "jq_int4_to_f6": (ctypes.c_int, [_vp, _i64, _i64, _vp, _vp]),
     "jq_int4_to_f6_weight": (ctypes.c_int, [_vp, _i64, _i64, _vp, _vp]),
     "jq_ternary_to_f6_weight": (ctypes.c_int, [_vp, _i64, _i64, _vp, _vp]),
@@ -454,6 +455,32 @@ def jq_w4a4_f6_linear(x, wf6, w_scale, bias=None, y=None, workspace=None, stream
                                  _stream_ptr(stream))
     _check(st, "jq_w4a4_f6_linear")
     return y
+
+
+JQ_QUANT_BATCH_MAX = 8
+
+
+def jq_quantize_act_f6_batch(xs, xf6s=None, scales=None, stream=None):
+    """Per-token BF6 quantisation of several independent bf16 [M_i, K_i] inputs in
+    one call; returns (list of BF6 operands, list of scales)."""
+    torch = _torch()
+    n = len(xs)
+    if xf6s is None:
+        xf6s = [torch.empty((jq_f6_operand_bytes(*x.shape),), dtype=torch.uint8, device=x.device) for x in xs]
+    if scales is None:
+        scales = [torch.empty((x.shape[0],), dtype=torch.float32, device=x.device) for x in xs]
+    if not (len(xf6s) == len(scales) == n):
+        raise ValueError("xs, xf6s and scales must have the same length")
+    ptrs = lambda vals: (ctypes.c_void_p * max(n, 1))(*[v.value for v in vals])
+    xp = ptrs([_dev(x, torch.bfloat16, None, f"xs[{i}]") for i, x in enumerate(xs)])
+    qp = ptrs([_dev(q, torch.uint8, (jq_f6_operand_bytes(*x.shape),), f"xf6s[{i}]")
+               for i, (x, q) in enumerate(zip(xs, xf6s))])
+    sp = ptrs([_dev(s, torch.float32, (x.shape[0],), f"scales[{i}]") for i, (x, s) in enumerate(zip(xs, scales))])
+    Ms = (ctypes.c_int64 * max(n, 1))(*[x.shape[0] for x in xs])
+    Ks = (ctypes.c_int64 * max(n, 1))(*[x.shape[1] for x in xs])
+    st = lib().jq_quantize_act_f6_batch(n, xp, Ms, Ks, qp, sp, _stream_ptr(stream))
+    _check(st, "jq_quantize_act_f6_batch")
+    return xf6s, scales
 
 
 # The library-held scratch of jq_w4a4_f6_linear_noalloc, per device (include/jq.h).

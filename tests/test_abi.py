@@ -31,7 +31,7 @@ def header_functions():
 
 def test_exports_every_declared_symbol():
     names = header_functions()
-    assert len(names) == 34, names
+    assert len(names) == 35, names
     lib = ctypes.CDLL(jq.LIB_PATH)
     for n in names:
         assert hasattr(lib, n), f"libjq.so does not export {n}"
@@ -232,6 +232,29 @@ def test_f6_gemm_and_linear_validation():
     assert L.jq_w4a4_f6_gemm_i32(A, 8, 64, A, 8, MIS, None) == jq.JQ_ERR_MISALIGNED
     # operands of 2 GiB or more are refused (31-bit buffer descriptors)
     assert L.jq_w4a4_f6_gemm_i32(A, 1 << 22, 65536, A, 8, A, None) == jq.JQ_ERR_UNSUPPORTED_SHAPE
+
+
+def test_f6_quantize_batch_validation():
+    # argument checks of the batched BF6 quantiser, all before anything is launched
+    f = jq.lib().jq_quantize_act_f6_batch
+    P = ctypes.c_void_p * 2
+    I = ctypes.c_int64 * 2
+
+    def call(n=2, x=(A, A), M=(8, 16), K=(64, 128), q=(A, A), s=(A, A)):
+        return f(n, P(*x), I(*M), I(*K), P(*q), P(*s), None)
+
+    assert call(n=0) == jq.JQ_ERR_INVALID_ARG
+    assert call(n=9) == jq.JQ_ERR_INVALID_ARG
+    assert f(2, None, I(8, 8), I(64, 64), P(A, A), P(A, A), None) == jq.JQ_ERR_INVALID_ARG
+    assert call(x=(A, None)) == jq.JQ_ERR_INVALID_ARG
+    assert call(q=(None, A)) == jq.JQ_ERR_INVALID_ARG
+    assert call(s=(A, None)) == jq.JQ_ERR_INVALID_ARG
+    assert call(M=(8, 0)) == jq.JQ_ERR_INVALID_ARG
+    assert call(K=(64, 96)) == jq.JQ_ERR_UNSUPPORTED_SHAPE
+    assert call(K=(65600, 64)) == jq.JQ_ERR_UNSUPPORTED_SHAPE
+    assert call(x=(A, MIS)) == jq.JQ_ERR_MISALIGNED
+    assert call(q=(A + 8, A)) == jq.JQ_ERR_MISALIGNED
+    assert call(s=(A, A + 2)) == jq.JQ_ERR_MISALIGNED
 
 
 def test_f6_linear_noalloc_validation():

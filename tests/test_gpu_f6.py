@@ -387,3 +387,50 @@ def test_f6_w158a4_linear_ragged(M, K, N, bias):
     y6, y8, wt, g = f6_ternary_layer(x, w, b)
     assert torch.equal(y6.view(torch.int16), y8.view(torch.int16))
     assert_bf16_close(jq.bf16_bits(y6), oracle.w158a4_linear(x, wt, g, b), f"f6 ternary {M}x{K}->{N}")
+
+
+# ---------------------------------------------------------------------------
+# Batched BF6 quantiser: several independent inputs in one call
+# ---------------------------------------------------------------------------
+
+
+@pytest.mark.parametrize("shapes", [
+    [(4608, 3072), (9216, 12288)],                                  # the FLUX MLP pair
+    [(1, 64), (33, 192), (4097, 256), (7, 16384), (5, 20480)],      # ragged rows; the last row is past 16384 codes
+    [(100 + 37 * i, 64 * (1 + 7 * i)) for i in range(8)],          # eight inputs
+    [(64, 4160)],                                                   # one input
+], ids=["flux_pair", "ragged_and_long", "eight", "single"])
+def test_quantize_f6_batch_matches_single_launches(shapes):
+    say("f6 quantise batch", shapes)
+    bits = [workloads.activations(M, K, "student_t3", 70 + i, 0.005, 50.0) for i, (M, K) in enumerate(shapes)]
+    xs = [dev_bf16(b) for b in bits]
+    qb, sb = jq.jq_quantize_act_f6_batch(xs)
+    torch.cuda.synchronize()
+    for i, (x, (M, K)) in enumerate(zip(xs, shapes)):
+        q1, s1 = jq.jq_quantize_act_f6(x)
+        torch.cuda.synchronize()
+        assert torch.equal(qb[i], q1), f"input {i} {M}x{K}: BF6 operand differs from its own launch"
+        assert torch.equal(sb[i].view(torch.int32), s1.view(torch.int32)), f"input {i}: scales differ"
+        if M * K <= 1 << 22:
+            rq, rs = oracle.quantize_act(bits[i])
+            assert np.array_equal(sb[i].cpu().numpy().view(np.uint32), rs.view(np.uint32))
+            assert np.array_equal(decode_f6(qb[i].cpu().numpy(), M, K), padded_codes(rq, M, K)), f"input {i}: codes"
+
+
+def test_quantize_f6_batch_outputs_feed_the_gemm():
+    """The FLUX MLP pair quantised in one call, then each linear's GEMM: the
+    outputs equal the whole layer's (jq_w4a4_f6_linear) bit for bit."""
+    lins = workloads.FLUX_MLP.linears
+    xs, ws, bs = [], [], []
+    for lin in lins:
+        xs.append(dev_bf16(lin.make_x()))
+        wq, sw = jq.jq_pack_weight_int4(dev_bf16(lin.make_w()))
+        ws.append((jq.jq_int4_to_f6_weight(wq), sw))
+        b = lin.make_bias()
+        bs.append(None if b is None else dev_bf16(b))
+    qs, ss = jq.jq_quantize_act_f6_batch(xs)
+    for lin, x, (wf6, sw), b, q, s in zip(lins, xs, ws, bs, qs, ss):
+        y1 = jq.jq_w4a4_f6_gemm(q, s, lin.K, wf6, sw, b)
+        y2 = jq.jq_w4a4_f6_linear(x, wf6, sw, b)
+        torch.cuda.synchronize()
+        assert torch.equal(y1.view(torch.int16), y2.view(torch.int16)), lin.name
