@@ -84,6 +84,18 @@ def parse_args():
     p.add_argument("--no-secondary", action="store_true", help="skip the secondary workloads")
     p.add_argument("--copy-calib", action="store_true",
                    help="also run a plain 256 MiB device copy (calibrates HBM byte counters under rocprofv3)")
+    p.add_argument("--secondary-filter", default="",
+                   help="run only the secondary cases whose workload or layer name contains this text")
+    p.add_argument("--operand-study", action="store_true",
+                   help="also time the dominant GEMM on all-zero, constant, workload and random codes")
+    p.add_argument("--full-rounds", action="store_true",
+                   help="also time both engines' GEMMs on 8192x12288 -> 4096, whose tiles fill whole rounds")
+    p.add_argument("--overlap-study", action="store_true",
+                   help="also time the step with the down-projection's quantiser on a second stream")
+    p.add_argument("--min-warm-steps", type=int, default=MIN_WARM_STEPS,
+                   help="warm-up floor in steps (lower it only for counter-collection runs, which "
+                        "serialise every launch)")
+    p.add_argument("--min-warm-seconds", type=float, default=MIN_WARM_SECONDS, help="warm-up floor in seconds")
     return p.parse_args()
 
 
@@ -133,7 +145,7 @@ class ClockMonitor:
     background thread; summary(t0, t1) reduces the samples taken between two
     perf_counter() times."""
 
-    def __init__(self, period_s=0.002):
+    def __init__(self, period_s=0.001):
         self.period = period_s
         self.samples = []
         self.error = None
@@ -150,20 +162,26 @@ class ClockMonitor:
             self.error = f"amdsmi unavailable: {e!r}"[:200]
 
     def read(self):
+        # amdsmi_get_clock_info reads the current GFX clock; the gpu-metrics
+        # table was seen to return stale values at this sampling rate
         if self._h is None:
-            return None
-        try:
-            m = self._amdsmi.amdsmi_get_gpu_metrics_info(self._h)
-        except Exception as e:  # noqa: BLE001
-            self.error = f"gpu metrics: {e!r}"[:200]
             return None
 
         def num(v):
-            return v if isinstance(v, (int, float)) else None
+            return v if isinstance(v, (int, float)) and v > 0 else None
 
-        xcd = [v for v in (m.get("current_gfxclks") or []) if isinstance(v, (int, float)) and 0 < v < 10000]
-        return {"t": time.perf_counter(), "gfx_mhz": num(m.get("current_gfxclk")),
-                "xcd_mhz": xcd, "power_w": num(m.get("current_socket_power"))}
+        rec = {"t": time.perf_counter(), "gfx_mhz": None, "power_w": None}
+        try:
+            rec["gfx_mhz"] = num(self._amdsmi.amdsmi_get_clock_info(self._h, self._amdsmi.AmdSmiClkType.GFX)
+                                 .get("clk"))
+        except Exception as e:  # noqa: BLE001
+            self.error = f"clock info: {e!r}"[:200]
+        try:
+            p = self._amdsmi.amdsmi_get_power_info(self._h)
+            rec["power_w"] = num(p.get("current_socket_power")) or num(p.get("average_socket_power"))
+        except Exception:  # noqa: BLE001
+            pass
+        return rec if rec["gfx_mhz"] is not None else None
 
     def _run(self):
         while not self._stop.is_set():
@@ -197,8 +215,6 @@ class ClockMonitor:
 
         out["gfx_mhz"] = stats("gfx_mhz", inside)
         out["power_w"] = stats("power_w", inside)
-        xcd = [sum(s["xcd_mhz"]) / len(s["xcd_mhz"]) for s in inside if s["xcd_mhz"]]
-        out["xcd_mean_mhz"] = None if not xcd else sum(xcd) / len(xcd)
         out["gfx_mhz_before"] = before[-1]["gfx_mhz"] if before else None
         out["gfx_mhz_after"] = after[0]["gfx_mhz"] if after else None
         if self.error:
@@ -517,7 +533,170 @@ def cpu_baseline(preps, target_s):
     return res
 
 
-def secondary(torch, jq, workloads, steps, warmup, n_launch):
+def operand_study(torch, jq, lin, prep, clock, launches=200):
+    """The bf6 GEMM of one linear (the MLP-down one: the dominant kernel) on
+    operands of different switching activity: all-zero codes, every code 1,
+    the workload's codes and uniformly random int4 codes (weights and
+    activations alike; random codes are re-encoded by the library's
+    converters).  A GEMM whose time does not depend on the data is bound by
+    its own structure, not by the chip's power limit."""
+    M, K, N = lin.M, lin.K, lin.N
+    g = torch.Generator(device="cuda")
+    g.manual_seed(5)
+    rnd_x = torch.randint(0, 256, (M, K // 2), dtype=torch.uint8, device="cuda", generator=g)
+    rnd_w = torch.randint(0, 256, (N, K // 2), dtype=torch.uint8, device="cuda", generator=g)
+    one_x = torch.full((M, K // 2), 0x11, dtype=torch.uint8, device="cuda")
+    one_w = torch.full((N, K // 2), 0x11, dtype=torch.uint8, device="cuda")
+    xq, xs = prep.quantize()
+    cases = {
+        "zero": (torch.zeros_like(xq), torch.zeros_like(prep.wq)),
+        "ones": (jq.jq_int4_to_f6(one_x), jq.jq_int4_to_f6_weight(one_w)),
+        "workload": (xq, prep.wq),
+        "random": (jq.jq_int4_to_f6(rnd_x), jq.jq_int4_to_f6_weight(rnd_w)),
+    }
+    del rnd_x, rnd_w, one_x, one_w
+    y = torch.empty((M, N), dtype=torch.bfloat16, device="cuda")
+    stream = torch.cuda.current_stream()
+    out = {}
+    for name, (xa, wa) in cases.items():
+        for _ in range(MIN_WARM_STEPS):
+            jq.jq_w4a4_f6_gemm(xa, xs, K, wa, prep.sw, None, y=y)
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        t0 = time.perf_counter()
+        e0.record(stream)
+        for _ in range(launches):
+            jq.jq_w4a4_f6_gemm(xa, xs, K, wa, prep.sw, None, y=y)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        us = e0.elapsed_time(e1) / launches * 1e3
+        out[name] = {"avg_us": us, "TOPS": lin.ops / us / 1e6, "clock": clock.summary(t0, t1)}
+        log(f"operand study {lin.name} {name}: {us:.1f} us, {lin.ops / us / 1e6:.0f} TOPS")
+    return {"linear": lin.name, "M": M, "K": K, "N": N, "launches": launches, "cases": out}
+
+
+def full_rounds(torch, jq, workloads, launches=100):
+    """Both engines' GEMMs on a shape whose output tiles fill whole rounds of
+    the chip's block slots (8192 x 12288 -> 4096: 512 tiles of 256 x 256 for
+    the bf6 engine's 256 one-block CUs, 1024 tiles of 128 x 256 for the int8
+    engine's 512 two-block slots), next to the FLUX MLP-down shape
+    (9216 x 12288 -> 3072), whose tiles leave the last round part-empty.
+    Inputs have the MLP-down statistics."""
+    base = workloads.FLUX_MLP.linears[1]
+    full = workloads.Linear("full_rounds_8192x12288x4096", M=8192, K=12288, N=4096, x_dist=base.x_dist,
+                            x_seed=base.x_seed, outlier_frac=base.outlier_frac,
+                            outlier_factor=base.outlier_factor, w_std=base.w_std, w_seed=base.w_seed)
+    stream = torch.cuda.current_stream()
+    out = []
+    for lin in (base, full):
+        p6 = Prepared(lin, torch, jq, "bf6")
+        p4 = Prepared(lin, torch, jq, "int4")
+        for eng, p in (("bf6", p6), ("int8", p4)):
+            qs = p.quantize()
+            for _ in range(MIN_WARM_STEPS):
+                p.gemm(*qs)
+            torch.cuda.synchronize()
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for _ in range(launches):
+                p.gemm(*qs)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            us = e0.elapsed_time(e1) / launches * 1e3
+            tops = lin.ops / us / 1e6
+            peak = PEAK_FP6_TOPS if eng == "bf6" else PEAK_INT8_TOPS
+            out.append({"linear": lin.name, "M": lin.M, "K": lin.K, "N": lin.N, "engine": eng, "avg_us": us,
+                        "TOPS": tops, "frac_mfma_peak": tops / peak, "pct_int8_peak": 100 * tops / PEAK_INT8_TOPS})
+            log(f"full rounds {lin.name} {eng}: {us:.1f} us, {tops:.0f} TOPS ({100 * tops / peak:.1f}% of its peak)")
+        del p6, p4
+        torch.cuda.empty_cache()
+    return out
+
+
+def workloads_mod():
+    from paper_2609_33601_amd import workloads
+
+    return workloads
+
+
+def overlap_study(torch, jq, preps, steps=200):
+    """The bf6 step with the down-projection's quantiser moved to a second
+    stream (equal priority), so that it can run beside the up-projection's
+    quantiser and GEMM, against the same step on one stream.  The inputs of
+    the two linears are independent, so the order is free."""
+    up, dn = preps
+    main = torch.cuda.current_stream()
+    side = torch.cuda.Stream()
+
+    def serial():
+        for p in preps:
+            p.gemm(*p.quantize())
+
+    def side_first():
+        e = torch.cuda.Event()
+        e.record(main)
+        side.wait_event(e)  # the previous step is done with the down operand
+        with torch.cuda.stream(side):
+            qd = dn.quantize()
+        up.gemm(*up.quantize())
+        e2 = torch.cuda.Event()
+        e2.record(side)
+        main.wait_event(e2)
+        dn.gemm(*qd)
+
+    def both_quantisers_first():
+        e = torch.cuda.Event()
+        e.record(main)
+        side.wait_event(e)
+        with torch.cuda.stream(side):
+            qd = dn.quantize()
+        qu = up.quantize()
+        e2 = torch.cuda.Event()
+        e2.record(side)
+        main.wait_event(e2)
+        up.gemm(*qu)
+        dn.gemm(*qd)
+
+    def batched():
+        # both inputs quantised in one launch (jq_quantize_act_f6_batch), then the GEMMs
+        (qu, qd), (su, sd) = jq.jq_quantize_act_f6_batch([up.x, dn.x], [up.q, dn.q], [up.s, dn.s])
+        up.gemm(qu, su)
+        dn.gemm(qd, sd)
+
+    # small inputs, where a launch's latency outweighs its bytes: the three
+    # distinct inputs of the 8B dLLM block (gate/up, o-proj, down) for 64
+    # tokens, quantised by three launches or by one
+    small = [lin for lin in workloads_mod().WORKLOADS["dllm_block"].linears if not lin.shares_input]
+    sx = [jq.bf16_tensor(lin.make_x()[:64], "cuda") for lin in small]
+    sq = [torch.empty((jq.jq_f6_operand_bytes(*x.shape),), dtype=torch.uint8, device="cuda") for x in sx]
+    ss = [torch.empty((x.shape[0],), dtype=torch.float32, device="cuda") for x in sx]
+
+    def small_separate():
+        for x, q, s_ in zip(sx, sq, ss):
+            jq.jq_quantize_act_f6(x, q, s_)
+
+    def small_batched():
+        jq.jq_quantize_act_f6_batch(sx, sq, ss)
+
+    out = {}
+    for name, fn in (("small inputs (3 x 64 tokens of the dLLM block): three launches", small_separate),
+                     ("small inputs (3 x 64 tokens of the dLLM block): one batched launch", small_batched)):
+        r = time_steps(torch, fn, steps, 20)
+        out[name] = {"us_per_step": r["us_per_step"], "per_step_us": r["per_step_us"]}
+        log(f"overlap study: {name}: {r['us_per_step']:.1f} us")
+    for name, fn in (("one stream", serial), ("down quantiser on a second stream, beside the up linear", side_first),
+                     ("both quantisers side by side, then the GEMMs", both_quantisers_first),
+                     ("both inputs quantised in one launch, then the GEMMs", batched)):
+        r = time_steps(torch, fn, steps, 20)
+        out[name] = {"us_per_step": r["us_per_step"], "per_step_us": r["per_step_us"]}
+        log(f"overlap study: {name}: {r['us_per_step']:.1f} us/step")
+    return out
+
+
+def secondary(torch, jq, workloads, steps, warmup, n_launch, only=""):
     cases = [(workloads.FLUX_MLP, "ternary_bf6"), (workloads.FLUX_MLP, "ternary"),
              (workloads.WORKLOADS["mlp_down_1img"], "bf6"), (workloads.WORKLOADS["mlp_down_1img"], "int4"),
              (workloads.WORKLOADS["dllm_block"], "bf6"), (workloads.WORKLOADS["dllm_block"], "int4"),
@@ -526,6 +705,11 @@ def secondary(torch, jq, workloads, steps, warmup, n_launch):
              (workloads.WORKLOADS["qkv"], "bf6"), (workloads.WORKLOADS["qkv"], "int4"),
              (workloads.FLUX_MLP, "group64_bf6"), (workloads.FLUX_MLP, "group64"),
              (workloads.WORKLOADS["dllm_block"], "group128_bf6"), (workloads.WORKLOADS["dllm_block"], "group128")]
+    layer_names = {"ternary": "W1.58A4 (int8 engine)", "ternary_bf6": "W1.58A4 (bf6 engine)",
+                   "int4": "W4A4 (int8 engine)", "bf6": "W4A4 (bf6 engine)",
+                   "group64": "W4A4 group64 (int8 engine)", "group128": "W4A4 group128 (int8 engine)",
+                   "group64_bf6": "W4A4 group64 (bf6 engine)", "group128_bf6": "W4A4 group128 (bf6 engine)"}
+    cases = [(wl, fmt) for wl, fmt in cases if not only or only in wl.name or only in layer_names[fmt]]
     out = []
     for wl, fmt in cases:
         check_shared_inputs(list(wl.linears))
@@ -533,10 +717,7 @@ def secondary(torch, jq, workloads, steps, warmup, n_launch):
         r = time_steps(torch, make_step(preps), steps, warmup)
         us = r["us_per_step"]
         tops = wl.ops / (us * 1e-6) / 1e12
-        layer = {"ternary": "W1.58A4 (int8 engine)", "ternary_bf6": "W1.58A4 (bf6 engine)",
-                 "int4": "W4A4 (int8 engine)", "bf6": "W4A4 (bf6 engine)",
-                 "group64": "W4A4 group64 (int8 engine)", "group128": "W4A4 group128 (int8 engine)",
-                 "group64_bf6": "W4A4 group64 (bf6 engine)", "group128_bf6": "W4A4 group128 (bf6 engine)"}[fmt]
+        layer = layer_names[fmt]
         per = per_linear_times(torch, preps, n_launch)
         rec = {"workload": wl.description, "layer": layer, "us_per_step": us, "effective_TOPS": tops,
                "pct_int8_peak": 100.0 * tops / PEAK_INT8_TOPS, "warmup_steps": r["warmup_steps"],
@@ -561,7 +742,9 @@ def secondary(torch, jq, workloads, steps, warmup, n_launch):
 
 
 def main():
+    global MIN_WARM_STEPS, MIN_WARM_SECONDS
     args = parse_args()
+    MIN_WARM_STEPS, MIN_WARM_SECONDS = args.min_warm_steps, args.min_warm_seconds
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the W4A4 linear "
               "shards without communication over tokens (M) and is measured at N=1.", file=sys.stderr)
@@ -656,9 +839,16 @@ def main():
         log(f"cpu oracle: {cpu['value']:.4f} TOPS on {cpu['cores']} threads; {cpu['sample']}; "
             f"gpu/oracle differing outputs: {cpu['gpu_outputs_differing_from_oracle']}")
 
+    study = None
+    if args.operand_study:
+        study = operand_study(torch, jq, wl.linears[1], preps[1], clock)
+    ovl = overlap_study(torch, jq, preps) if args.overlap_study else None
+    fr = full_rounds(torch, jq, workloads) if args.full_rounds else None
+
     sec = None
     if not args.no_secondary:
-        sec = secondary(torch, jq, workloads, max(10, min(args.steps, 50)), args.warmup, 20)
+        sec = secondary(torch, jq, workloads, max(10, min(args.steps, 50)), args.warmup, 20,
+                        args.secondary_filter)
     clock.stop()
 
     props = torch.cuda.get_device_properties(0)
@@ -670,6 +860,7 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "warmup_steps_run": head["warmup_steps"],
+        "warmup_floor": {"steps": MIN_WARM_STEPS, "seconds": MIN_WARM_SECONDS},
         "ms_per_step": ms_per_step,
         "per_step_us": head["per_step_us"],
         "higher_is_better": True,
@@ -688,6 +879,8 @@ def main():
             "device": f"{props.name} {getattr(props, 'gcnArchName', '')} CUs={props.multi_processor_count}",
         },
         "clock": head.get("clock"),
+        "clock_note": "amdsmi readings (refreshed by the driver far less often than the sampling period; "
+                      "the effective clock of a kernel is in profiles/counters_flux_mlp.md)",
         "cold": {**cold, "effective_TOPS_median": wl.ops / (cold["per_step_us"]["median"] * 1e-6) / 1e12},
         "engines": {
             "bf6": {"us_per_step": head["us_per_step"], "effective_TOPS": value,
@@ -706,6 +899,12 @@ def main():
         "kernels": kernels,
         "secondary": sec,
     }
+    if study is not None:
+        out["operand_study"] = study
+    if ovl is not None:
+        out["overlap_study"] = ovl
+    if fr is not None:
+        out["full_rounds"] = fr
     print(json.dumps(out), flush=True)
 
 
