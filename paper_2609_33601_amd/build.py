@@ -1,7 +1,10 @@
 """Build libjq.so (the gfx950 HIP library behind include/jq.h) in-tree with hipcc.
 
 Each source compiles to its own object in parallel (_build/), then one hipcc
-link makes the shared library.  Every call compiles every source.
+link makes the shared library.  Every call compiles every source.  Alongside,
+the BF6 kernels are compiled to device assembly once more and their
+hand-ordered vector loads are checked (check_waits.py); a failed check fails
+the build.
 """
 
 import os
@@ -9,6 +12,11 @@ import shutil
 import subprocess
 import sys
 from concurrent.futures import ThreadPoolExecutor
+
+try:
+    from . import check_waits
+except ImportError:  # run as a script
+    import check_waits
 
 PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
@@ -21,6 +29,8 @@ ARCH = "gfx950"
 # Per-source flags: the BF6 kernels are built without machine sinking, which
 # would move the first k-step's MFMAs of a GEMM stage below its barrier.
 SOURCE_FLAGS = {"f6.hip": ["-mllvm", "-disable-machine-sink"]}
+# Sources whose GEMM's asm-issued loads are checked against their waits.
+CHECKED_SOURCES = ("f6.hip",)
 
 HIPCC_FLAGS = [
     f"--offload-arch={ARCH}",
@@ -61,9 +71,15 @@ def build(verbose=False, extra_flags=(), jobs=None):
     objs = [os.path.join(OBJ_DIR, os.path.splitext(s)[0] + ".o") for s in SOURCES]
     cmds = [[cc, *HIPCC_FLAGS, *SOURCE_FLAGS.get(s, []), *extra_flags, *inc, "-c", os.path.join(CSRC, s), "-o", o]
             for s, o in zip(SOURCES, objs)]
-    jobs = jobs or max(1, min(len(cmds), os.cpu_count() or 1))
+    checked = [s for s in SOURCES if s in CHECKED_SOURCES]
+    jobs = jobs or max(1, min(len(cmds) + len(checked), os.cpu_count() or 1))
     with ThreadPoolExecutor(max_workers=jobs) as pool:
-        for f in [pool.submit(_run, c, verbose) for c in cmds]:
+        futs = [pool.submit(_run, c, verbose) for c in cmds]
+        futs += [pool.submit(check_waits.compile_and_check,
+                             [cc, *HIPCC_FLAGS, *SOURCE_FLAGS.get(s, []), *extra_flags, *inc],
+                             os.path.join(CSRC, s), os.path.join(OBJ_DIR, os.path.splitext(s)[0] + ".s"))
+                 for s in checked]
+        for f in futs:
             f.result()
     tmp = LIB + ".tmp"
     _run([cc, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp], verbose)

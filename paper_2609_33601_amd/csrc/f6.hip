@@ -70,28 +70,36 @@
 //     sets (so the stage loop is unrolled by six, a multiple of both ring
 //     sizes).
 //   * Per stage: the eight MFMAs of k-step 0 run while the wave reads its
-//     k-step 1 fragments from LDS; then it waits for its share of the next
-//     stage's DMA, meets the others at a barrier (no memory fence) and issues
-//     the DMA three stages ahead into the slot just read; then the MFMAs of
-//     k-step 1 run while the next stage's k-step 0 fragments are read.  No
-//     VALU work sits between the MFMAs.
+//     k-step 1 fragments from LDS and issues the next stage's weight loads,
+//     one or two after each fragment's MFMAs; then it waits for its share
+//     of the next stage's DMA and meets the others at a barrier (no memory
+//     fence); then the MFMAs of k-step 1 run while the next stage's k-step 0
+//     fragments are read and the DMA three stages ahead goes into the slot
+//     just read, one instruction after each of the first fragments.  Issued
+//     in one burst per wave at the stage's start and middle, the same loads
+//     queued up behind each other and held the waves' MFMAs back (the
+//     spread issue took the FLUX MLP-down GEMM from 147 to 131 us on zero
+//     codes).  No VALU work sits between the MFMAs.
 //   * Every vector-memory instruction of the stage loop (the weight loads
 //     and the buffer -> LDS transfers) is issued as an instruction of its
 //     own, and the loop orders it with explicit waits only: at a stage's
-//     start, after issuing the next stage's weights, vmcnt(9) (this stage's
-//     weights have landed); at its middle, vmcnt(9), lgkmcnt(0) and the
+//     start, vmcnt(3) (this stage's weights, issued before the previous
+//     stage's DMA, have landed); at its middle, vmcnt(9), lgkmcnt(0) and the
 //     barrier (the next slot's DMA has landed and every read of the slot
 //     about to be refilled has completed).  Left to the compiler, the
 //     transfers made it wait for every DMA in flight before each LDS read.
-//     The file is also built without machine sinking, which otherwise moved
-//     the first k-step's MFMAs below the stage's barrier (into the block
-//     after the tile's first-stage branch), leaving the matrix pipes idle
-//     while both waves of a SIMD waited there.
-//   * Operands reach the MFMAs without register copies: a band's three
-//     weight loads of a stage fill 12 consecutive registers, whose first
-//     and last six are the two k-steps' operands, and an activation
-//     fragment's 16- and 8-byte parts land next to each other (the 8-byte
-//     part read on its own, not paired with another fragment's).
+//     The compiler does not know that these loads complete after they
+//     issue, so the loaded registers pass through an empty asm after their
+//     wait before any use, and the build checks the generated code: no
+//     instruction may touch a load's registers before a wait retires it
+//     (check_waits.py).  The file is also built without machine sinking,
+//     which otherwise moved the first k-step's MFMAs below the stage's
+//     barrier (into the block after the tile's first-stage branch), leaving
+//     the matrix pipes idle while both waves of a SIMD waited there.
+//   * An activation fragment's 16- and 8-byte parts land next to each other
+//     in registers (the 8-byte part read on its own, not paired with another
+//     fragment's), and a band's three 16-byte weight parts of a stage are
+//     the two k-steps' operands as two overlapping 6-dword windows.
 //   * The weight fragment is operand A and the activation fragment operand B,
 //     so the 32x32 result is y^T: lane L holds column m = L % 32 and rows
 //     n = 8j + 4(L / 32) + r (j, r = 0..3).  The epilogue scales them, packs
@@ -103,6 +111,7 @@
 #include <algorithm>
 #include <mutex>
 #include <type_traits>
+#include <utility>
 
 #include "gemm_common.h"
 #include "jq.h"
@@ -589,12 +598,21 @@ struct WFrag {
 // A wave's weights of one stage as loaded: three 16-byte parts per band
 // (the six dwords of k-step 0, then those of k-step 1), turned into MFMA
 // operands only once the stage's wait has passed.
-typedef int v12i __attribute__((ext_vector_type(12)));
 struct WRaw {
-  v12i p[2];  // [band]: the three parts in load order
+  v4i32 p[2][3];  // [band][part]
 };
 
 __device__ __forceinline__ v8i join(v4i32 a, v2i32 b) { return v8i{a.x, a.y, a.z, a.w, b.x, b.y, 0, 0}; }
+
+// f(integral_constant<int, i>) for i = 0 .. N - 1, in order, as straight-line code.
+template <typename F, int... I>
+__device__ __forceinline__ void static_for_impl(F&& f, std::integer_sequence<int, I...>) {
+  (f(std::integral_constant<int, I>{}), ...);
+}
+template <int N, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  static_for_impl(f, std::make_integer_sequence<int, N>{});
+}
 
 // Buffer -> LDS transfers issued as instructions of their own (M0 set
 // alongside), so that the compiler neither tracks them nor orders LDS reads
@@ -724,35 +742,35 @@ __global__ __launch_bounds__(64 * WAVES, 8 / WAVES) void w4a4_f6_gemm_kernel(
       (WAVES == 4 && static_cast<int>(blockIdx.x / kNumXcd) >= grid_blocks / kNumXcd / 2) ? T / 2 : 0;
   auto rot = [&](int st) __attribute__((always_inline)) { return st + koff < T ? st + koff : st + koff - T; };
 
-  // Stage `st` of the tile at (m0, n0): activations into slot k, weights into w.
-  auto issue_dma = [&](int m0, int st, int k) __attribute__((always_inline)) {
+  // Stage `st` of the tile at (m0, n0): part j of the wave's share of its
+  // activations into slot k, or part pp (band pp / 3, 16-byte part pp % 3)
+  // of its weights into w.
+  auto issue_dma = [&](int m0, int st, int k, int j) __attribute__((always_inline)) {
     uint4* dst = slot(k) + 64 * kDmaPerWave * wave;
-#pragma unroll
-    for (int j = 0; j < kDmaPerWave; ++j) {
-      const uint32_t band = static_cast<uint32_t>(min(m0 / 32 + rband[j], mbands - 1));
-      dma16_raw(rsx, lds_addr(dst + 64 * j), rpart[j] == kOutside ? kOutside : band * band_bytes + rpart[j],
-                2 * kFragBytes * rot(st));
-    }
+    const uint32_t band = static_cast<uint32_t>(min(m0 / 32 + rband[j], mbands - 1));
+    dma16_raw(rsx, lds_addr(dst + 64 * j), rpart[j] == kOutside ? kOutside : band * band_bytes + rpart[j],
+              2 * kFragBytes * rot(st));
   };
-  auto load_w = [&](WRaw& w, int n0, int st) __attribute__((always_inline)) {
-#pragma unroll
-    for (int f = 0; f < 2; ++f) {
-      const uint32_t wb = static_cast<uint32_t>(min(n0 / 32 + 2 * wn + f, nbands - 1)) * band_bytes;
-      const uint32_t so = static_cast<uint32_t>(2 * rot(st) * kFragBytes);
-      const v4i32 p0 = load16_raw(rsw, wb + 16 * lane, so);
-      const v4i32 p1 = load16_raw(rsw, wb + 1024 + 16 * lane, so);
-      const v4i32 p2 = load16_raw(rsw, wb + 2048 + 16 * lane, so);
-      w.p[f] = v12i{p0.x, p0.y, p0.z, p0.w, p1.x, p1.y, p1.z, p1.w, p2.x, p2.y, p2.z, p2.w};
-    }
+  auto load_w = [&](WRaw& w, int n0, int st, int pp) __attribute__((always_inline)) {
+    const int f = pp / 3, q = pp % 3;
+    const uint32_t wb = static_cast<uint32_t>(min(n0 / 32 + 2 * wn + f, nbands - 1)) * band_bytes;
+    const uint32_t so = static_cast<uint32_t>(2 * rot(st) * kFragBytes);
+    w.p[f][q] = load16_raw(rsw, wb + 1024 * q + 16 * lane, so);
   };
-  // the MFMA operands of a loaded stage (after the wait for its loads)
-  auto frags = [&](const WRaw& w) __attribute__((always_inline)) {
+  // The MFMA operands of a loaded stage, once the wait for its loads has
+  // passed.  The compiler takes an asm load's result as ready when the asm
+  // is issued, so the parts first pass through an empty asm placed after the
+  // wait: any copy it makes to assemble an operand then reads them after the
+  // wait, not in the register a load may still be writing.
+  auto frags = [&](WRaw& w) __attribute__((always_inline)) {
+    asm volatile("" : "+v"(w.p[0][0]), "+v"(w.p[0][1]), "+v"(w.p[0][2]), "+v"(w.p[1][0]), "+v"(w.p[1][1]),
+                 "+v"(w.p[1][2]));
     WFrag r;
 #pragma unroll
     for (int f = 0; f < 2; ++f) {
       // the k-steps are the 6-dword windows of the 12 loaded dwords
-      r.f[0][f] = __builtin_shufflevector(w.p[f], w.p[f], 0, 1, 2, 3, 4, 5, -1, -1);
-      r.f[1][f] = __builtin_shufflevector(w.p[f], w.p[f], 6, 7, 8, 9, 10, 11, -1, -1);
+      r.f[0][f] = __builtin_shufflevector(w.p[f][0], w.p[f][1], 0, 1, 2, 3, 4, 5, -1, -1);
+      r.f[1][f] = __builtin_shufflevector(w.p[f][1], w.p[f][2], 2, 3, 4, 5, 6, 7, -1, -1);
     }
     return r;
   };
@@ -836,20 +854,23 @@ __global__ __launch_bounds__(64 * WAVES, 8 / WAVES) void w4a4_f6_gemm_kernel(
   WRaw w0, w1;
   {
     int m0, n0, st;
-    load_w(w0, cn0, 0);
-    issue_dma(cm0, 0, 0);
+    static_for<kWLoads>([&](auto PP) __attribute__((always_inline)) { load_w(w0, cn0, 0, decltype(PP)::value); });
+    static_for<kDmaPerWave>([&](auto J) __attribute__((always_inline)) { issue_dma(cm0, 0, 0, decltype(J)::value); });
     ahead(0, 0, 1, &m0, &n0, &st);
-    issue_dma(m0, st, 1);
+    static_for<kDmaPerWave>([&](auto J) __attribute__((always_inline)) { issue_dma(m0, st, 1, decltype(J)::value); });
     ahead(0, 0, 2, &m0, &n0, &st);
-    issue_dma(m0, st, 2);
+    static_for<kDmaPerWave>([&](auto J) __attribute__((always_inline)) { issue_dma(m0, st, 2, decltype(J)::value); });
   }
   __builtin_amdgcn_s_waitcnt(vmcnt_imm(2 * kDmaPerWave));  // DMA(0)
   __builtin_amdgcn_s_barrier();
   __builtin_amdgcn_sched_barrier(0);
   // A wave's activation fragments of a stage, (k-step s, band fm) in order
-  // 4s + fm, roll through a window of four: fragment i is read while the
-  // MFMAs of fragment i - 4 run.
-  v8i bq0 = read_b(0, 0, 0), bq1 = read_b(0, 0, 1), bq2 = read_b(0, 0, 2), bq3 = read_b(0, 0, 3);
+  // nfm s + fm, roll through a window of nfm register sets: fragment i is
+  // read (into the set fragment i - nfm has just left) while the MFMAs of
+  // fragment i - nfm run.
+  v8i bq[4];
+#pragma unroll
+  for (int fm = 0; fm < nfm; ++fm) bq[fm] = read_b(0, 0, fm);
 
   // Epilogue of the current tile: lane holds column m = m0 + 128 wm + 32 fm +
   // (lane & 31) and rows n = n0 + 64 wn + 32 f + 8 j + 4 (lane >> 5) + r of
@@ -979,66 +1000,70 @@ __global__ __launch_bounds__(64 * WAVES, 8 / WAVES) void w4a4_f6_gemm_kernel(
   };
 
   // One stage g = g0 + I, g0 a multiple of 6: slot I % 3 and weight set
-  // I % 2, both known at compile time; t is its stage within tile ti.  The
-  // stage starts by loading stage g + 1's weights into the other set (done
-  // with at stage g - 1).  Half way through, once every wave has read the
-  // whole slot (lgkmcnt(0) + barrier) and DMA(g + 1) has landed, the slot
-  // takes the DMA of stage g + 3 (at a tile's first stage, the tile's scales
-  // are moved first).  The wait there, vmcnt(kWLoads + kDmaPerWave) = 9,
-  // leaves in flight at most the loads issued since stage g's weights:
-  // DMA(g + 2) and stage g + 1's weights.  Vector loads complete in order,
-  // so DMA(g + 1), issued before those, has landed (the stores of an
-  // epilogue in between only add to the count).  After a tile's last stage
-  // comes its epilogue.
+  // I % 2, both known at compile time; t is its stage within tile ti.
+  //   * At its start, the wait for this stage's weights (loaded during the
+  //     previous stage's first k-step): vmcnt(kDmaPerWave) leaves in flight
+  //     only the DMA issued after them (vector loads complete in order).
+  //   * Then the stage's fragments j = nfm s + fm (k-step s, band fm) in
+  //     turn: the two MFMAs of fragment j, the read of fragment j + nfm into
+  //     the register set fragment j has left (past the stage's last
+  //     fragment, those of the next stage, from the next slot), and a share
+  //     of the stage's vector-memory loads, so that they reach the memory
+  //     system spread over the stage rather than in one burst per wave:
+  //     stage g + 1's weights (into the other set, done with at stage g - 1)
+  //     among the first k-step's fragments, and the DMA of stage g + 3
+  //     among the second's.
+  //   * Between the k-steps, once every wave has read the whole slot
+  //     (lgkmcnt(0) + barrier) and DMA(g + 1) has landed, the slot is free
+  //     for that DMA (at a tile's first stage, the tile's scales are moved
+  //     first).  The wait there, vmcnt(kWLoads + kDmaPerWave) = 9, leaves in
+  //     flight at most the loads issued since this stage's weights (which
+  //     have landed): DMA(g + 2) and stage g + 1's weights.  DMA(g + 1),
+  //     issued before them, has therefore landed (the stores of an epilogue
+  //     in between only add to the count).
+  // After a tile's last stage comes its epilogue.
   WRaw* wset[2] = {&w0, &w1};
   int t = 0, ti = 0;
   auto stage = [&](auto I) __attribute__((always_inline)) {
     constexpr int i = decltype(I)::value;
     constexpr int cur = i % 3, nxt = (i + 1) % 3;
-    {
-      int m0, n0, st;
-      ahead(t, ti, 1, &m0, &n0, &st);
-      load_w(*wset[(i + 1) % 2], n0, st);
-    }
-    // This stage's weights (loaded at the previous stage) have landed once at
-    // most the loads issued since are in flight: the DMA issued at the
-    // previous stage's barrier and the weights just issued (vector loads
-    // complete in order).  The same wait covers the DMA issued one barrier
-    // earlier still (it is older).
-    __builtin_amdgcn_s_waitcnt(vmcnt_imm(kWLoads + kDmaPerWave));
+    int wm0, wn0, wst, dm0 = 0, dst = 0;  // the tile and stage of the weights and the DMA issued here
+    ahead(t, ti, 1, &wm0, &wn0, &wst);
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(kDmaPerWave));
     __builtin_amdgcn_sched_barrier(0);
     const WFrag wc = frags(*wset[i % 2]);
-#define JQ_F6_STEP(S, FM, BQ, NK, NS, NFM)                                                              \
-  if constexpr (FM < nfm) {                                                                             \
-    acc[0][FM] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(wc.f[S][0], BQ, acc[0][FM], 3, 3, 0, 127, \
-                                                                  0, 127);                              \
-    acc[1][FM] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(wc.f[S][1], BQ, acc[1][FM], 3, 3, 0, 127, \
-                                                                  0, 127);                              \
-  }                                                                                                     \
-  if constexpr (NFM < nfm) BQ = read_b(NK, NS, NFM);
-    // k-step 0; the window moves on to k-step 1 of this stage
-    JQ_F6_STEP(0, 0, bq0, cur, 1, 0)
-    JQ_F6_STEP(0, 1, bq1, cur, 1, 1)
-    JQ_F6_STEP(0, 2, bq2, cur, 1, 2)
-    JQ_F6_STEP(0, 3, bq3, cur, 1, 3)
-    __builtin_amdgcn_sched_barrier(0);
-    __builtin_amdgcn_s_waitcnt(kLgkm0);
-    __builtin_amdgcn_s_waitcnt(vmcnt_imm(kWLoads + kDmaPerWave));
-    __builtin_amdgcn_s_barrier();
-    __builtin_amdgcn_sched_barrier(0);
-    if (t == 0) issue_scales(cm0, cn0);
-    {
-      int m0, n0, st;
-      ahead(t, ti, 3, &m0, &n0, &st);
-      issue_dma(m0, st, cur);
-    }
-    // k-step 1; the window moves on to k-step 0 of the next stage (past the
-    // block's last stage these reads are of a slot whose data is not used)
-    JQ_F6_STEP(1, 0, bq0, nxt, 0, 0)
-    JQ_F6_STEP(1, 1, bq1, nxt, 0, 1)
-    JQ_F6_STEP(1, 2, bq2, nxt, 0, 2)
-    JQ_F6_STEP(1, 3, bq3, nxt, 0, 3)
-#undef JQ_F6_STEP
+    static_for<2 * nfm>([&](auto J) __attribute__((always_inline)) {
+      constexpr int j = decltype(J)::value;
+      constexpr int ks = j / nfm, fm = j % nfm, r = j + nfm;
+      acc[0][fm] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(wc.f[ks][0], bq[fm], acc[0][fm], 3, 3, 0, 127, 0,
+                                                                   127);
+      acc[1][fm] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(wc.f[ks][1], bq[fm], acc[1][fm], 3, 3, 0, 127, 0,
+                                                                   127);
+      if constexpr (r < 2 * nfm) bq[fm] = read_b(cur, 1, fm);
+      else bq[fm] = read_b(nxt, 0, fm);
+      if constexpr (ks == 0) {
+        // weight parts pp with pp nfm / kWLoads == j
+        static_for<kWLoads>([&](auto PP) __attribute__((always_inline)) {
+          constexpr int pp = decltype(PP)::value;
+          if constexpr (pp * nfm / kWLoads == j) load_w(*wset[(i + 1) % 2], wn0, wst, pp);
+        });
+      } else if constexpr (fm < kDmaPerWave) {
+        issue_dma(dm0, dst, cur, fm);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      if constexpr (j == nfm - 1) {
+        __builtin_amdgcn_s_waitcnt(kLgkm0);
+        __builtin_amdgcn_s_waitcnt(vmcnt_imm(kWLoads + kDmaPerWave));
+        __builtin_amdgcn_s_barrier();
+        __builtin_amdgcn_sched_barrier(0);
+        if (t == 0) issue_scales(cm0, cn0);
+        int dn0;
+        ahead(t, ti, 3, &dm0, &dn0, &dst);
+      }
+    });
+    // (past the block's last stage the reads of the next slot are of data
+    // that is not used)
+    static_assert(kDmaPerWave <= 3, "the DMA parts go with the second k-step's fragments");
     __builtin_amdgcn_sched_barrier(0);
     if (t == last) {
       if (T == 1) {

@@ -225,7 +225,8 @@ def f6_i32(qx, qw):
 
 @pytest.mark.parametrize("M,N,K", [(1, 1, 64), (3, 5, 128), (32, 32, 64), (257, 255, 192),
                                    (300, 520, 1024), (256, 256, 3072), (513, 1000, 640),
-                                   (1, 4099, 128), (2049, 3, 320), (512, 768, 12288)])
+                                   (1, 4099, 128), (2049, 3, 320), (512, 768, 12288),
+                                   (300, 777, 6912), (2048, 2048, 7680)])
 def test_f6_gemm_i32_random_codes(M, N, K):
     say("f6 gemm i32", M, N, K)
     qx = rand_packed(M, K, seed=M * 7 + K)
@@ -236,7 +237,8 @@ def test_f6_gemm_i32_random_codes(M, N, K):
     assert bad.size == 0, f"{len(bad)} accumulators differ, first {bad[:4].tolist()}"
 
 
-@pytest.mark.parametrize("M,N,K", [(4096, 8192, 384), (2100, 9000, 448), (4608, 4096, 256), (300, 70000, 512)])
+@pytest.mark.parametrize("M,N,K", [(4096, 8192, 384), (2100, 9000, 448), (4608, 4096, 256), (300, 70000, 512),
+                                   (2100, 9000, 6912), (4096, 8192, 6912)])
 def test_f6_gemm_i32_several_tiles_per_block(M, N, K):
     """More tiles than CUs: blocks walk several tiles, with loads running
     ahead across tile boundaries (three or more stages per tile), or one tile
@@ -299,7 +301,8 @@ def test_f6_linear_tiny_workload(with_bias):
 
 
 @pytest.mark.parametrize("M,K,N,bias", [(77, 3072, 130, True), (1, 64, 1, False), (5, 192, 4096, True),
-                                        (300, 1088, 260, False), (513, 256, 777, True), (257, 4160, 300, True)])
+                                        (300, 1088, 260, False), (513, 256, 777, True), (257, 4160, 300, True),
+                                        (300, 6912, 777, True), (513, 7680, 1000, True), (2048, 6912, 520, False)])
 def test_f6_linear_ragged(M, K, N, bias):
     say("f6 linear ragged", M, K, N, bias)
     x = workloads.activations(M, K, "student_t3", M + 3, 0.01, 50.0)
