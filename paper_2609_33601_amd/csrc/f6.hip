@@ -1109,9 +1109,13 @@ __global__ __launch_bounds__(64 * WAVES, 8 / WAVES) void w4a4_f6_gemm_kernel(
 // owns activation bands 2wm, 2wm + 1 and weight bands 2wn, 2wn + 1 of the
 // tile: 2 x 2 tiles of 32x32, 64 fp32 sums per lane.  A stage is 128 codes of
 // K: both operands' fragments (activation layout and weight layout, 12 KiB
-// each) move into LDS by buffer_load ... lds, one stage ahead, into two
-// slots; the stage's scales (s_x and s_w of its groups, gathered from the
-// [rows, K/G] arrays) follow through registers.  Operand bands past M or N
+// each) and the stage's scales (s_x and s_w of its groups, gathered from the
+// [rows, K/G] arrays by 4-byte transfers) move into LDS by buffer_load ...
+// lds, issued as instructions of their own two stages ahead into a ring of
+// three slots.  A stage waits only for its own loads (vmcnt counts the next
+// stage's as still in flight) and then meets the other waves at a barrier
+// with no memory fence, after which the slot read two stages ago takes the
+// loads of the stage two ahead.  Operand bands, rows or columns past M or N
 // read as zero (outside the buffers).
 template <int G, Epilogue EPI, bool HAS_BIAS>
 __global__ __launch_bounds__(256, 2) void w4a4g_f6_gemm_kernel(
@@ -1120,16 +1124,16 @@ __global__ __launch_bounds__(256, 2) void w4a4g_f6_gemm_kernel(
     const uint16_t* __restrict__ bias, void* __restrict__ out, int tiles_m, int tiles_n) {
   constexpr int kGps = 128 / G;                    // groups per stage
   constexpr int kOpU4 = 4 * 2 * kFragBytes / 16;   // one operand's stage: 4 bands x 3072 bytes
-  // Two slots: the operand fragments of a stage (activations, then weights)
-  // and its scales (s_x, then s_w).  Accesses name the slot array directly,
-  // with the slot known at compile time, so that the compiler can tell the
-  // slot being read from the one the DMA is filling.
-  __shared__ uint4 op0[2 * kOpU4];
-  __shared__ uint4 op1[2 * kOpU4];
-  __shared__ float sc0[2 * kGps * 128];
-  __shared__ float sc1[2 * kGps * 128];
-  auto opk = [&](int k) __attribute__((always_inline)) { return k == 0 ? op0 : op1; };
-  auto sck = [&](int k) __attribute__((always_inline)) { return k == 0 ? sc0 : sc1; };
+  constexpr int kScF = 2 * kGps * 128;             // one stage's scales: s_x then s_w, [group][row]
+  constexpr int kScDma = kScF / 64 / 4;            // 4-byte scale transfers per wave per stage
+  constexpr int kLoads = 6 + kScDma;               // vector-memory instructions per wave per stage
+  // Three slots, each the operand fragments of a stage (activations, then
+  // weights) and its scales.  The transfers are asm the compiler does not
+  // track, so the slot may be computed at run time.
+  __shared__ uint4 ops[3 * 2 * kOpU4];
+  __shared__ float scs[3 * kScF];
+  auto opk = [&](int k) __attribute__((always_inline)) { return ops + 2 * kOpU4 * k; };
+  auto sck = [&](int k) __attribute__((always_inline)) { return scs + kScF * k; };
 
   TileCoord tc;
   if (!tile_of_block(blockIdx.x, tiles_m, tiles_n, &tc)) return;
@@ -1141,10 +1145,10 @@ __global__ __launch_bounds__(256, 2) void w4a4g_f6_gemm_kernel(
   const int T = ksteps / 2;
   const uint32_t band_bytes = static_cast<uint32_t>(ksteps) * kFragBytes;
 
-  const __amdgpu_buffer_rsrc_t rsx = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<uint8_t*>(xf6), 0, static_cast<int>(static_cast<int64_t>(mbands) * band_bytes), kBufferFlags);
-  const __amdgpu_buffer_rsrc_t rsw = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<uint8_t*>(wf6), 0, static_cast<int>(static_cast<int64_t>(nbands) * band_bytes), kBufferFlags);
+  const RawRsrc rsx = raw_rsrc(xf6, static_cast<uint32_t>(static_cast<int64_t>(mbands) * band_bytes));
+  const RawRsrc rsw = raw_rsrc(wf6, static_cast<uint32_t>(static_cast<int64_t>(nbands) * band_bytes));
+  const RawRsrc rssx = raw_rsrc(sx, static_cast<uint32_t>(4 * static_cast<int64_t>(M) * KG));
+  const RawRsrc rssw = raw_rsrc(sw, static_cast<uint32_t>(4 * static_cast<int64_t>(N) * KG));
 
   // Operand DMA: the 12 KiB of a stage are 12 instructions of 1 KiB, three
   // per wave; instruction i = 3 wave + j is part i % 3 of band i / 3.  Bands
@@ -1158,37 +1162,37 @@ __global__ __launch_bounds__(256, 2) void w4a4g_f6_gemm_kernel(
     xoff[j] = xb < mbands ? static_cast<uint32_t>(xb) * band_bytes + 1024 * part + 16 * lane : kOutside;
     woff[j] = wb < nbands ? static_cast<uint32_t>(wb) * band_bytes + 1024 * part + 16 * lane : kOutside;
   }
+  // Scale DMA: entry e of a stage's kScF (s_x entries, then s_w) is group
+  // e % (kGps 128) / 128 of row (column) e % 128 of the tile; instruction
+  // i = kScDma wave + j moves entries 64 i .. 64 i + 63, all of one array.
+  // Per lane: the array's row and the group within the stage; entries past
+  // M or N read as zero.
+  int sc_row[kScDma], sc_gl[kScDma];
+  bool sc_w[kScDma];  // wave-uniform: whether instruction j moves s_w entries
+#pragma unroll
+  for (int j = 0; j < kScDma; ++j) {
+    sc_w[j] = 64 * (kScDma * wave + j) >= kGps * 128;
+    const int ee = (64 * (kScDma * wave + j) + lane) % (kGps * 128);
+    sc_gl[j] = ee / 128;
+    sc_row[j] = (sc_w[j] ? n0 : m0) + ee % 128;
+  }
   auto issue = [&](int u, int k) __attribute__((always_inline)) {
-    uint4* const xa = opk(k);
-    uint4* const wa = opk(k) + kOpU4;
-    const int so = 2 * kFragBytes * u;
+    const uint32_t xa = lds_addr(opk(k)), wa = lds_addr(opk(k) + kOpU4);
+    const uint32_t so = 2 * kFragBytes * u;
 #pragma unroll
     for (int j = 0; j < 3; ++j) {
-      dma16(rsx, xa + 64 * (3 * wave + j), xoff[j], so);  // kOutside + so stays outside
-      dma16(rsw, wa + 64 * (3 * wave + j), woff[j], so);
+      dma16_raw(rsx, xa + 16 * 64 * (3 * wave + j), xoff[j], so);  // kOutside + so stays outside
+      dma16_raw(rsw, wa + 16 * 64 * (3 * wave + j), woff[j], so);
     }
-  };
-  // The stage's scales, kGps * 128 of s_x and of s_w (entry e: group e / 128
-  // of row, or column, e % 128 of the tile; zero past M, N or K), go through
-  // registers: loaded with the stage's DMA, written to the scale slot once
-  // they have landed.  (Moved by DMA as well, some of their reads lost the
-  // alias information that tells the slots apart, and every such read
-  // waited for the next stage's DMA.)
-  float scv[2];
-  auto load_scales = [&](int u) __attribute__((always_inline)) {
-    if constexpr (kGps == 2) {
-      const int gl = tid >> 7, r = tid & 127, g = 2 * u + gl;
-      scv[0] = (m0 + r < M && g < KG) ? sx[static_cast<int64_t>(m0 + r) * KG + g] : 0.0f;
-      scv[1] = (n0 + r < N && g < KG) ? sw[static_cast<int64_t>(n0 + r) * KG + g] : 0.0f;
-    } else {
-      const int r = tid & 127;
-      if (tid < 128) scv[0] = m0 + r < M ? sx[static_cast<int64_t>(m0 + r) * KG + u] : 0.0f;
-      else scv[0] = n0 + r < N ? sw[static_cast<int64_t>(n0 + r) * KG + u] : 0.0f;
+#pragma unroll
+    for (int j = 0; j < kScDma; ++j) {
+      const int g = kGps * u + sc_gl[j];
+      const bool in = sc_row[j] < (sc_w[j] ? N : M) && g < KG;
+      const uint32_t off = in ? 4u * static_cast<uint32_t>(sc_row[j] * KG + g) : kOutside;
+      const uint32_t dst = lds_addr(sck(k) + 64 * (kScDma * wave + j));
+      if (sc_w[j]) dma4_raw(rssw, dst, off);
+      else dma4_raw(rssx, dst, off);
     }
-  };
-  auto store_scales = [&](int k) __attribute__((always_inline)) {
-    sck(k)[tid] = scv[0];
-    if constexpr (kGps == 2) sck(k)[256 + tid] = scv[1];
   };
 
   v16f S[2][2];  // [weight band f][activation band fb]
@@ -1198,10 +1202,8 @@ __global__ __launch_bounds__(256, 2) void w4a4g_f6_gemm_kernel(
     for (int fb = 0; fb < 2; ++fb) S[f][fb] = v16f{};
 
   // Fold one group into the sums: lane holds column m = 32 (2wm + fb) +
-  // (lane & 31) and rows n = 32 (2wn + f) + 8 j + 4 (lane >> 5) + r of y^T.
-  // The lane's scales of a stage, read from the scale slot before the next
-  // stage's DMA is issued (some of these reads lose the alias information
-  // that tells the slots apart and would otherwise wait for that DMA).
+  // (lane & 31) and rows n = 32 (2wn + f) + 8 j + 4 (lane >> 5) + r of y^T,
+  // with the lane's scales of the stage read from its scale slot.
   float xsr[kGps][2];
   float4 wsr[kGps][2][4];
   auto read_scales = [&](int k) __attribute__((always_inline)) {
@@ -1278,31 +1280,23 @@ __global__ __launch_bounds__(256, 2) void w4a4g_f6_gemm_kernel(
     }
   };
 
-  // Two stages per iteration, one per slot: wait for the stage's loads,
-  // write its scales, meet at a barrier (every wave is then also done with
-  // the other slot), issue the next stage into the other slot, compute.
-  load_scales(0);
+  // Stage u from slot u % 3: wait for its loads (those of stage u + 1, issued
+  // after them, may still be in flight: vector loads complete in order),
+  // meet the other waves (every wave is then also done with slot (u - 1) % 3,
+  // read at the previous stage), issue stage u + 2 into that slot, compute.
   issue(0, 0);
-  for (int u = 0; u < T; u += 2) {
-    __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
-    store_scales(0);
-    __syncthreads();
-    read_scales(0);
-    if (u + 1 < T) {
-      load_scales(u + 1);  // before the DMA: a wait for them then counts past it
-      issue(u + 1, 1);
-    }
-    compute(u, 0);
-    if (u + 1 >= T) break;
-    __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
-    store_scales(1);
-    __syncthreads();
-    read_scales(1);
-    if (u + 2 < T) {
-      load_scales(u + 2);
-      issue(u + 2, 0);
-    }
-    compute(u + 1, 1);
+  if (T > 1) issue(1, 1);
+  for (int u = 0; u < T; ++u) {
+    const int k = u % 3;
+    if (u + 1 < T) __builtin_amdgcn_s_waitcnt(vmcnt_imm(kLoads));
+    else __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+    __builtin_amdgcn_s_barrier();
+    // no LDS read of the slot may be moved above the wait and the barrier
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_sched_barrier(0);
+    if (u + 2 < T) issue(u + 2, (u + 2) % 3);
+    read_scales(k);
+    compute(u, k);
   }
 
   if constexpr (EPI == Epilogue::kF32) {
@@ -1333,7 +1327,7 @@ __global__ __launch_bounds__(256, 2) void w4a4g_f6_gemm_kernel(
     // wave two passes of 32 rows x 64 columns, 16-byte chunk c of row r at
     // chunk c ^ ((r >> 1) & 7).
     __syncthreads();
-    v4u32* stg = reinterpret_cast<v4u32*>(op0) + 256 * wave;
+    v4u32* stg = reinterpret_cast<v4u32*>(ops) + 256 * wave;
     v2u32* stg2 = reinterpret_cast<v2u32*>(stg);
     float bv[2][4][4];
 #pragma unroll
