@@ -2,9 +2,9 @@
 
 Each source compiles to its own object in parallel (_build/), then one hipcc
 link makes the shared library.  Every call compiles every source.  Alongside,
-the BF6 kernels are compiled to device assembly once more and their
-hand-ordered vector loads are checked (check_waits.py); a failed check fails
-the build.
+the BF6 kernels are compiled to device assembly once more and the GEMM's
+hand-ordered vector loads are checked against their waits (check_waits.py); a
+failed check fails the build.
 """
 
 import os
@@ -29,8 +29,9 @@ ARCH = "gfx950"
 # Per-source flags: the BF6 kernels are built without machine sinking, which
 # would move the first k-step's MFMAs of a GEMM stage below its barrier.
 SOURCE_FLAGS = {"f6.hip": ["-mllvm", "-disable-machine-sink"]}
-# Sources whose GEMM's asm-issued loads are checked against their waits.
-CHECKED_SOURCES = ("f6.hip",)
+# Sources whose asm-issued loads are checked against their waits, and the
+# kernel names checked in each.
+CHECKED_SOURCES = {"f6.hip": "w4a4_f6_gemm_kernel"}
 
 HIPCC_FLAGS = [
     f"--offload-arch={ARCH}",
@@ -77,7 +78,8 @@ def build(verbose=False, extra_flags=(), jobs=None):
         futs = [pool.submit(_run, c, verbose) for c in cmds]
         futs += [pool.submit(check_waits.compile_and_check,
                              [cc, *HIPCC_FLAGS, *SOURCE_FLAGS.get(s, []), *extra_flags, *inc],
-                             os.path.join(CSRC, s), os.path.join(OBJ_DIR, os.path.splitext(s)[0] + ".s"))
+                             os.path.join(CSRC, s), os.path.join(OBJ_DIR, os.path.splitext(s)[0] + ".s"),
+                             CHECKED_SOURCES[s])
                  for s in checked]
         for f in futs:
             f.result()

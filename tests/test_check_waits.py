@@ -1,6 +1,7 @@
-"""The build's check of the BF6 GEMM's hand-ordered vector loads (check_waits.py),
-on hand-written assembly: it must flag every touch of a load's destination
-registers that no vmcnt wait has retired, and nothing else."""
+"""The build's check of the BF6 GEMM's hand-ordered vector loads
+(check_waits.py), on hand-written assembly: along every control-flow path it
+must flag each touch of a load's destination registers that no vmcnt wait has
+retired, and nothing else."""
 
 import pytest
 
@@ -51,8 +52,45 @@ def test_lds_dma_has_no_destination_registers():
 
 def test_loop_wrap():
     # a load at the bottom of the loop body, read at its top with no wait between
-    assert len(run("\tv_mov_b32_e32 v8, v4\n"
-                   "\tbuffer_load_dwordx4 v[4:7], v0, s[0:3], s4 offen\n")) >= 1
+    body = (".LBB0_1:\n"
+            "\tv_mov_b32_e32 v8, v4\n"
+            "\tbuffer_load_dwordx4 v[4:7], v0, s[0:3], s4 offen\n"
+            "\ts_cbranch_scc1 .LBB0_1\n")
+    assert len(run(body)) >= 1
+    # the same with the wait at the top of the loop is clean
+    assert run(body.replace(".LBB0_1:\n", ".LBB0_1:\n\ts_waitcnt vmcnt(0)\n")) == []
+
+
+def test_out_of_line_block_is_checked_where_it_runs():
+    # a block placed after the load in the text but reached only from before it
+    body = ("\ts_cbranch_scc1 .LBB0_9\n"
+            ".LBB0_2:\n"
+            "\tbuffer_load_dwordx4 v[4:7], v0, s[0:3], s4 offen\n"
+            "\ts_waitcnt vmcnt(0)\n"
+            "\ts_endpgm\n"
+            ".LBB0_9:\n"
+            "\tv_mov_b32_e32 v4, 1\n"
+            "\ts_branch .LBB0_2\n")
+    assert run(body) == []
+    # reached from after the load instead: flagged
+    body2 = ("\tbuffer_load_dwordx4 v[4:7], v0, s[0:3], s4 offen\n"
+             "\ts_cbranch_scc1 .LBB0_9\n"
+             "\ts_waitcnt vmcnt(0)\n"
+             "\ts_endpgm\n"
+             ".LBB0_9:\n"
+             "\tv_mov_b32_e32 v4, 1\n"
+             "\ts_endpgm\n")
+    assert len(run(body2)) == 1
+
+
+def test_paths_merge_conservatively():
+    # waited for on one path only: still pending where the paths meet
+    body = ("\tbuffer_load_dwordx4 v[4:7], v0, s[0:3], s4 offen\n"
+            "\ts_cbranch_scc1 .LBB0_3\n"
+            "\ts_waitcnt vmcnt(0)\n"
+            ".LBB0_3:\n"
+            "\tv_mov_b32_e32 v8, v5\n")
+    assert len(run(body)) == 1
 
 
 def test_check_asm_raises_and_counts():

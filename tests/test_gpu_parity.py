@@ -219,6 +219,21 @@ def test_gemm_i32_random_codes(M, N, K):
     assert bad.size == 0, f"{len(bad)} accumulators differ, first {bad[:4].tolist()}"
 
 
+# Many tiles (more than one round of blocks), ragged M and N, short and
+# medium K.
+@pytest.mark.parametrize("M,N,K", [(4096, 8192, 384), (2100, 9000, 512), (300, 70000, 512), (2049, 3, 384),
+                                   (4608, 4096, 1152), (9216, 3072, 640), (33, 4099, 1536)])
+def test_gemm_i32_many_tiles(M, N, K):
+    say("gemm i32 many tiles", M, N, K)
+    qx = rand_packed(M, K, seed=M * 5 + K)
+    qw = rand_packed(N, K, seed=N * 3 + K)
+    acc = jq.jq_w4a4_gemm_i32(torch.from_numpy(qx).cuda(), torch.from_numpy(qw).cuda())
+    torch.cuda.synchronize()
+    ref = oracle.w4a4_gemm_i32(qx, qw)
+    bad = np.argwhere(acc.cpu().numpy() != ref)
+    assert bad.size == 0, f"{len(bad)} accumulators differ, first {bad[:4].tolist()}"
+
+
 @pytest.mark.parametrize("code_x,code_w", [(-8, -8), (7, -8), (-7, 7)])
 def test_gemm_i32_extreme_codes_max_k(code_x, code_w):
     K = 65536
@@ -257,7 +272,9 @@ def test_linear_tiny_workload_full(with_bias):
 
 
 @pytest.mark.parametrize("M,K,N,bias", [(77, 3072, 130, True), (1, 64, 1, False), (5, 192, 4096, True),
-                                        (300, 1088, 260, False), (513, 256, 777, True)])
+                                        (300, 1088, 260, False), (513, 256, 777, True),
+                                        (513, 1024, 777, True), (300, 6912, 777, True), (2048, 6912, 520, False),
+                                        (4100, 384, 2050, True)])
 def test_linear_ragged(M, K, N, bias):
     say("linear ragged", M, K, N, bias)
     x = workloads.activations(M, K, "student_t3", M + 3, 0.01, 50.0)
