@@ -733,13 +733,17 @@ __global__ __launch_bounds__(64 * WAVES, 8 / WAVES) void w4a4_f6_gemm_kernel(
     rpart[j] = (R % S::kBands) < tile_bands ? (R / S::kBands) * kFragBytes + 16 * q : kOutside;
   }
   const uint32_t band_bytes = static_cast<uint32_t>(ksteps) * kFragBytes;
-  // With two blocks per CU, the second half of each XCD's blocks walks the
-  // stages of its tiles from the middle of K (the fp32 sums of integers do
-  // not depend on the order), so the two blocks on a CU reach their
-  // epilogues half a tile apart and one runs its MFMAs while the other
-  // stores.
+  // The blocks walk the stages of their tiles from a point of K of their
+  // own (the fp32 sums of integers do not depend on the order).  One block
+  // per CU: each XCD starts an eighth of K after the one before, so that at
+  // any moment the XCDs read different slices of the operands rather than
+  // all requesting the same weight lines together.  Two blocks per CU: the
+  // second half of each XCD's blocks starts from the middle of K, so the two
+  // blocks on a CU reach their epilogues half a tile apart and one runs its
+  // MFMAs while the other stores.
   const int koff =
-      (WAVES == 4 && static_cast<int>(blockIdx.x / kNumXcd) >= grid_blocks / kNumXcd / 2) ? T / 2 : 0;
+      WAVES == 8 ? static_cast<int>(blockIdx.x % kNumXcd) * T / kNumXcd
+                 : ((static_cast<int>(blockIdx.x / kNumXcd) >= grid_blocks / kNumXcd / 2) ? T / 2 : 0);
   auto rot = [&](int st) __attribute__((always_inline)) { return st + koff < T ? st + koff : st + koff - T; };
 
   // Stage `st` of the tile at (m0, n0): part j of the wave's share of its
