@@ -989,7 +989,7 @@ __global__ __launch_bounds__(64 * WAVES, 8 / WAVES) void w4a4_f6_gemm_kernel(
           uint16_t* p = o + static_cast<int64_t>(m) * N + n;
           if (m >= mlim) {
           } else if (vec) {
-            *reinterpret_cast<uint4*>(p) = v;
+            __builtin_nontemporal_store(vv, reinterpret_cast<v4u32*>(p));
           } else {
             const uint32_t w[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
@@ -1375,7 +1375,7 @@ __global__ __launch_bounds__(256, 2) void w4a4g_f6_gemm_kernel(
         uint16_t* p = static_cast<uint16_t*>(out) + static_cast<int64_t>(m) * N + n;
         if (m >= M) {
         } else if (vec) {
-          *reinterpret_cast<uint4*>(p) = make_uint4(vv.x, vv.y, vv.z, vv.w);
+          __builtin_nontemporal_store(vv, reinterpret_cast<v4u32*>(p));
         } else {
           const uint32_t w[4] = {vv.x, vv.y, vv.z, vv.w};
 #pragma unroll

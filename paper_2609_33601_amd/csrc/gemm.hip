@@ -368,7 +368,7 @@ __global__ __launch_bounds__(kThreads, 2) void w4a4_gemm_kernel(
       uint16_t* p = o + static_cast<int64_t>(m) * N + n;
       if (m >= M) {
       } else if (vec) {
-        *reinterpret_cast<uint4*>(p) = make_uint4(v.x, v.y, v.z, v.w);
+        __builtin_nontemporal_store(v, reinterpret_cast<v4u32*>(p));
       } else {
         const uint32_t w[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
