@@ -15,7 +15,7 @@ import pytest
 import oracle
 from paper_2609_33601_amd import jq, workloads
 from tests import oracle_pins_group as PG
-from tests.test_gpu_parity import _edge_rows, _gpu, _sample_rows, assert_bf16_close, dev_bf16, say  # noqa: F401
+from tests.test_gpu_parity import _edge_rows, _gpu, assert_bf16_close, dev_bf16, say  # noqa: F401
 
 pytestmark = pytest.mark.gpu
 
@@ -178,30 +178,3 @@ def test_group_linear_edge_rows(G):
     b = workloads.bias(N, 0.01, 7)
     y, wq, sw = _layer(x, w, b, G)
     assert_bf16_close(y, oracle.w4a4g_linear(x, wq, sw, G, b), f"group{G} edge rows")
-
-
-@pytest.mark.parametrize("lin,G", _flux_dit(), ids=lambda v: getattr(v, "name", str(v)))
-def test_group_linear_full_size_sampled(lin, G):
-    """Full-size group-wise layer as the benchmark launches it; sampled rows vs the oracle."""
-    say("group linear full", lin.name, lin.M, lin.K, lin.N, G)
-    x_bits, w_bits, b_bits = lin.make_x(), lin.make_w(), lin.make_bias()
-    wq, sw = jq.jq_pack_weight_int4_group(dev_bf16(w_bits), G)
-    b = None if b_bits is None else dev_bf16(b_bits)
-    ws = torch.empty(jq.jq_w4a4g_workspace_bytes(lin.M, lin.K, G), dtype=torch.uint8, device="cuda")
-    y = jq.jq_w4a4g_linear(dev_bf16(x_bits), wq, sw, G, b, workspace=ws)
-    codes = lin.M * lin.K // 2
-    qx_dev = ws[:codes].view(lin.M, lin.K // 2)
-    off = (codes + 255) // 256 * 256
-    sx_dev = ws[off: off + lin.M * (lin.K // G) * 4].view(torch.float32).view(lin.M, lin.K // G)
-    S = jq.jq_w4a4g_gemm_f32(qx_dev, sx_dev, wq, sw, G)
-    torch.cuda.synchronize()
-    rows = _sample_rows(lin.M, seed=lin.N + G)
-    idx = torch.from_numpy(rows).cuda()
-    rq, rs = oracle.pack_weight_int4_group(w_bits, G)
-    assert np.array_equal(wq.cpu().numpy(), rq) and np.array_equal(sw.cpu().numpy().view(np.uint32), rs.view(np.uint32))
-    rqx, rsx = oracle.quantize_act_group(x_bits[rows], G)
-    assert np.array_equal(qx_dev[idx].cpu().numpy(), rqx), "workspace codes differ"
-    assert np.array_equal(sx_dev[idx].cpu().numpy().view(np.uint32), rsx.view(np.uint32)), "workspace scales differ"
-    ref_S = oracle.w4a4g_gemm_f32(rqx, rsx, rq, rs, G)
-    assert np.array_equal(S[idx].cpu().numpy().view(np.uint32), ref_S.view(np.uint32)), "fp32 group sums differ"
-    assert_bf16_close(jq.bf16_bits(y[idx]), oracle.group_epilogue(ref_S, b_bits), f"{lin.name} group{G}")
