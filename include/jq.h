@@ -484,6 +484,15 @@ jq_status jq_w4a4_f6_gemm_i32(const void* xf6, int64_t M, int64_t K,
                               const void* wf6, int64_t N, int32_t* acc, void* stream);
 
 /*
+ * The tile height the int8 engine's GEMM (jq_w4a4_gemm, _linear, _gemm_i32 and
+ * their W1.58A4 forms) takes for an M x K by K x N product on a device with
+ * `cus` compute units, for checking and tuning: *tile_rows = 128 or 112 rows
+ * of activations per output tile (256 columns).  Host-only; launches nothing.
+ * Errors: JQ_ERR_INVALID_ARG, JQ_ERR_UNSUPPORTED_SHAPE.
+ */
+jq_status jq_gemm_plan(int64_t M, int64_t N, int64_t K, int cus, int* tile_rows);
+
+/*
  * The block shape the BF6 GEMM (jq_w4a4_f6_gemm, _linear, _gemm_i32) takes for
  * an M x K by K x N product on a device with `cus` compute units, for checking
  * and tuning: *waves = 8 (one 8-wave block per CU) or 4 (two 4-wave blocks per

@@ -12,6 +12,9 @@
 //    block needs 64 KiB of LDS and at most 256 registers per lane, so two
 //    blocks share a CU and each SIMD runs two waves from different blocks:
 //    while one block waits at its barrier or on LDS, the other issues MFMAs.
+//    Where 128-row tiles would leave the last round of blocks mostly empty
+//    (FLUX MLP-down: 864 tiles over 512 slots), the launcher takes 112-row
+//    tiles instead (seven fragments of 16 rows; 996 tiles, two full rounds).
 //  * gfx950 has no int4 MFMA, so codes are widened to int8 for
 //    v_mfma_i32_16x16x64_i8.  Widening is VALU work, and VALU instructions
 //    between MFMAs slow the matrix pipe of the SIMD (measured with two waves
@@ -55,6 +58,9 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <algorithm>
+#include <initializer_list>
+
 #include "gemm_common.h"
 #include "jq_internal.h"
 
@@ -67,14 +73,12 @@ using namespace gemm_detail;
 typedef unsigned v4u32 __attribute__((ext_vector_type(4)));
 typedef unsigned v2u32 __attribute__((ext_vector_type(2)));
 
-constexpr int kBM = 128;       // activation rows per block
 constexpr int kBN = 256;       // weight rows per block
-constexpr int kXSlots = kBM * kXChunks;      // 16-byte slots of the int8 activation tile
-constexpr int kWM = 128, kWN = 64;           // per-wave tile: all activation rows, a quarter of the weight rows
-constexpr int kFM = kWM / 16, kFN = kWN / 16;
-constexpr int kXLoads = kBM * kChunks / kThreads;  // 16-byte activation loads per thread per stage
+constexpr int kWN = 64;        // per-wave tile: all activation rows of the block, a quarter of the weight rows
+constexpr int kFN = kWN / 16;
+constexpr int kXLoads = 2;     // 16-byte activation loads per thread per stage (rows r and r + 64)
 
-static_assert(kXLoads == 2, "activation staging below assumes two loads per thread");
+static_assert(128 * kChunks / kThreads == kXLoads, "activation staging assumes at most two loads per thread");
 
 // Weight formats.  kInt4: codes -8..7, two per byte (the W4A4 layer).
 // kTernary: codes -1..1, four per byte as 2-bit fields (the W1.58A4 layer).
@@ -89,7 +93,6 @@ struct WTraits {
   static constexpr int kStageBytes = 16 * kWChunks;
   static constexpr int kDmaRows = 64 / kWChunks;
   static constexpr int kDma = kWN / kDmaRows;          // weight DMA instructions per wave per stage
-  static constexpr int kStageSlots = kXSlots + kBN * kWChunks;
   static constexpr int kShift = kTern ? 10 : 8;
   static constexpr int kUnpackValu = kTern ? 7 : 6;    // VALU instructions per widened weight fragment
 };
@@ -123,13 +126,19 @@ __device__ __forceinline__ v4i unpack8_tern_order(uint32_t p0, uint32_t p1) {
   return r;
 }
 
-template <WeightFormat WF, Epilogue EPI, bool HAS_BIAS, bool KTAIL>
+// BM: activation rows per block tile, 128 or 112 (seven 16-row fragments,
+// for shapes whose 128-row tiles leave the last round of blocks mostly
+// empty; the launcher picks it).
+template <WeightFormat WF, Epilogue EPI, bool HAS_BIAS, bool KTAIL, int BM>
 __global__ __launch_bounds__(kThreads, 2) void w4a4_gemm_kernel(
     const uint8_t* __restrict__ qx, const float* __restrict__ sx, int M, int K,
     const uint8_t* __restrict__ qw, const float* __restrict__ sw, int N,
     const uint16_t* __restrict__ bias, void* __restrict__ out, int tiles_m, int tiles_n) {
   using WT = WTraits<WF>;
-  constexpr int kStageSlots = WT::kStageSlots, kWDma = WT::kDma;
+  static_assert(BM == 128 || BM == 112, "tile heights of 7 or 8 fragments");
+  constexpr int kBM = BM, kWM = BM, kFM = BM / 16;
+  constexpr int kXSlots = kBM * kXChunks;  // 16-byte slots of the int8 activation tile
+  constexpr int kStageSlots = kXSlots + kBN * WT::kWChunks, kWDma = WT::kDma;
   // Two stage buffers, each the int8 activation tile followed by the packed
   // weight tile; the bf16 epilogue reuses them to stage the output tile.
   constexpr int kOutSlots = kThreads / 64 * kWM * kWN * 2 / 16;
@@ -171,8 +180,10 @@ __global__ __launch_bounds__(kThreads, 2) void w4a4_gemm_kernel(
   }
   // Activation loads: thread loads packed chunk (tid & 3) of tile rows
   // (tid >> 2) + 64 i; it widens chunk c into int8 chunks 2c and 2c + 1.
+  // With 112-row tiles the last wave (rows 112..127) has no second load.
   const int xl_chunk = tid & 3;
   const int xl_row = tid >> 2;
+  const bool x2 = xl_row + 64 < kBM;  // wave-uniform
   uint32_t ox[kXLoads];
 #pragma unroll
   for (int i = 0; i < kXLoads; ++i)
@@ -195,7 +206,8 @@ __global__ __launch_bounds__(kThreads, 2) void w4a4_gemm_kernel(
     const uint32_t xback = (KTAIL && kb + 16 * xl_chunk >= row_bytes) ? 32u : 0u;
 #pragma unroll
     for (int i = 0; i < kXLoads; ++i)
-      gx[i] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rsx, ox[i] - xback, kb, 0));
+      if (i == 0 || x2)
+        gx[i] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rsx, ox[i] - xback, kb, 0));
     if (KTAIL && kb + 16 * xl_chunk >= row_bytes) {
 #pragma unroll
       for (int i = 0; i < kXLoads; ++i) gx[i] = make_uint4(0, 0, 0, 0);
@@ -205,6 +217,7 @@ __global__ __launch_bounds__(kThreads, 2) void w4a4_gemm_kernel(
 #pragma unroll
     for (int i = 0; i < kXLoads; ++i) {
       const int row = xl_row + 64 * i;
+      if (i == 1 && !x2) break;
       if constexpr (WT::kTern) {
         buf[x_slot(row, 2 * xl_chunk)] = __builtin_bit_cast(uint4, unpack8_tern_order(gx[i].x, gx[i].y));
         buf[x_slot(row, 2 * xl_chunk + 1)] = __builtin_bit_cast(uint4, unpack8_tern_order(gx[i].z, gx[i].w));
@@ -381,10 +394,41 @@ __global__ __launch_bounds__(kThreads, 2) void w4a4_gemm_kernel(
 
 }  // namespace
 
+// Tile height of the GEMM, 128 or 112 activation rows, for an M x N output
+// with `slots` block slots (two per CU).  The blocks of an XCD take its share
+// of the tiles in rounds of its slots.  A round costs one tile time when more
+// than half of the XCD's slots hold a block, about 0.6 of one when at most
+// half do (a lone block has its CU's matrix pipes to itself), nothing when
+// empty; a 112-row tile takes about 0.93 of a 128-row one.  The cheaper
+// estimate wins, 128 on ties.  (Measured: FLUX MLP-down 9216 x 12288 -> 3072
+// and the DiT projections gain 5-8% from 112-row tiles; the 8B dLLM linears,
+// whose 128-row tiles fill whole rounds, and FLUX MLP-up, whose last round
+// is three-eighths full, lose.)
+int gemm_tile_rows(int64_t M, int64_t N, int64_t slots) {
+  const int64_t tiles_n = (N + kBN - 1) / kBN;
+  const int64_t xcd_slots = std::max<int64_t>(1, slots / kNumXcd);
+  int best = 128;
+  int64_t best_cost = -1;
+  for (const int bm : {128, 112}) {
+    const int64_t per_xcd = ((M + bm - 1) / bm * tiles_n + kNumXcd - 1) / kNumXcd;
+    const int64_t rest = per_xcd % xcd_slots;
+    const int64_t tenths = 10 * (per_xcd / xcd_slots) + (rest == 0 ? 0 : 2 * rest <= xcd_slots ? 6 : 10);
+    const int64_t cost = tenths * (bm == 128 ? 100 : 93);
+    if (best_cost < 0 || cost < best_cost) best = bm, best_cost = cost;
+  }
+  return best;
+}
+
 hipError_t launch_w4a4_gemm(Epilogue epi, const uint8_t* qx, const float* sx, int64_t M, int64_t K,
                             const uint8_t* qw, const float* sw, int64_t N, const uint16_t* bias,
                             void* out, hipStream_t st, WeightFormat wf) {
-  const int tiles_m = static_cast<int>((M + kBM - 1) / kBM);
+  int dev = 0, cus = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+  if (e != hipSuccess) return e;
+  const int bm = gemm_tile_rows(M, N, 2 * std::max<int64_t>(kNumXcd, cus / kNumXcd * kNumXcd));
+  const int tiles_m = static_cast<int>((M + bm - 1) / bm);
   const int tiles_n = static_cast<int>((N + kBN - 1) / kBN);
   const int64_t T = static_cast<int64_t>(tiles_m) * tiles_n;
   const int64_t per_xcd = (T + kNumXcd - 1) / kNumXcd;
@@ -392,9 +436,15 @@ hipError_t launch_w4a4_gemm(Epilogue epi, const uint8_t* qx, const float* sx, in
   const dim3 block(kThreads);
   const int Mi = static_cast<int>(M), Ki = static_cast<int>(K), Ni = static_cast<int>(N);
   const bool tail = (K % 128) != 0;
-#define JQ_LAUNCH(W, E, B, T)                                                                      \
-  hipLaunchKernelGGL((w4a4_gemm_kernel<W, E, B, T>), grid, block, 0, st, qx, sx, Mi, Ki, qw, sw, Ni, \
-                     bias, out, tiles_m, tiles_n)
+#define JQ_LAUNCH(W, E, B, T)                                                                                \
+  do {                                                                                                       \
+    if (bm == 112)                                                                                           \
+      hipLaunchKernelGGL((w4a4_gemm_kernel<W, E, B, T, 112>), grid, block, 0, st, qx, sx, Mi, Ki, qw, sw, Ni, \
+                         bias, out, tiles_m, tiles_n);                                                       \
+    else                                                                                                     \
+      hipLaunchKernelGGL((w4a4_gemm_kernel<W, E, B, T, 128>), grid, block, 0, st, qx, sx, Mi, Ki, qw, sw, Ni, \
+                         bias, out, tiles_m, tiles_n);                                                       \
+  } while (0)
 #define JQ_DISPATCH(W)                                                                    \
   if (epi == Epilogue::kInt32) {                                                          \
     if (tail) JQ_LAUNCH(W, Epilogue::kInt32, false, true);                                \

@@ -518,6 +518,16 @@ jq_status jq_w4a4g_f6_gemm_f32(const void* xf6, const float* scales, int64_t M, 
                                            nullptr, s_f32, as_stream(stream)));
 }
 
+jq_status jq_gemm_plan(int64_t M, int64_t N, int64_t K, int cus, int* tile_rows) {
+  if (tile_rows == nullptr || cus < 1) return JQ_ERR_INVALID_ARG;
+  jq_status st = check_shape(M, K);
+  if (st != JQ_OK) return st;
+  st = check_shape(N, K);
+  if (st != JQ_OK) return st;
+  *tile_rows = jq::gemm_tile_rows(M, N, 2 * std::max<int64_t>(8, cus / 8 * 8));
+  return JQ_OK;
+}
+
 jq_status jq_f6_gemm_plan(int64_t M, int64_t N, int64_t K, int cus, int* waves, int* tile_rows) {
   if (waves == nullptr || tile_rows == nullptr || cus < 1) return JQ_ERR_INVALID_ARG;
   const jq_status st = check_f6_operands(M, N, K);

@@ -38,6 +38,9 @@ enum class WeightFormat { kInt4, kTernary };
 hipError_t launch_w4a4_gemm(Epilogue epi, const uint8_t* qx, const float* sx, int64_t M, int64_t K,
                             const uint8_t* qw, const float* sw, int64_t N, const uint16_t* bias,
                             void* out, hipStream_t st, WeightFormat wf = WeightFormat::kInt4);
+// Its tile height (128 or 112 activation rows) for an M x N output with
+// `slots` block slots (two per CU).
+int gemm_tile_rows(int64_t M, int64_t N, int64_t slots);
 
 // Group-wise GEMM: scales sx [M, K/G] and sw [N, K/G]; epi is kBf16 or kF32.
 hipError_t launch_w4a4g_gemm(Epilogue epi, const uint8_t* qx, const float* sx, int64_t M, int64_t K, int G,

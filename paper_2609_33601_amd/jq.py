@@ -52,6 +52,7 @@ SIGNATURES = {
     "jq_w4a4_f6_gemm": (ctypes.c_int, [_vp, _fp, _i64, _i64, _vp, _fp, _i64, _vp, _vp, _vp]),
     "jq_w4a4_f6_gemm_i32": (ctypes.c_int, [_vp, _i64, _i64, _vp, _i64, _ip, _vp]),
     "jq_f6_gemm_plan": (ctypes.c_int, [_i64, _i64, _i64, ctypes.c_int, _ip, _ip]),
+    "jq_gemm_plan": (ctypes.c_int, [_i64, _i64, _i64, ctypes.c_int, _ip]),
     "jq_quantize_act_group_f6": (ctypes.c_int, [_vp, _i64, _i64, _i64, _vp, _fp, _vp]),
     "jq_w4a4g_f6_workspace_bytes": (ctypes.c_size_t, [_i64, _i64, _i64]),
     "jq_w4a4g_f6_linear": (ctypes.c_int, [_vp, _i64, _i64, _i64, _vp, _fp, _i64, _vp, _vp, _vp, _sz, _vp]),
@@ -382,6 +383,14 @@ def jq_f6_operand_bytes(rows, K):
 
 def jq_w4a4_f6_workspace_bytes(M, K):
     return int(lib().jq_w4a4_f6_workspace_bytes(int(M), int(K)))
+
+
+def jq_gemm_plan(M, N, K, cus):
+    """Tile rows (128 or 112) the int8 engine's GEMM takes for an M x K by K x N product on `cus` CUs (host only)."""
+    t = ctypes.c_int(0)
+    st = lib().jq_gemm_plan(int(M), int(N), int(K), int(cus), ctypes.byref(t))
+    _check(st, "jq_gemm_plan")
+    return t.value
 
 
 def jq_f6_gemm_plan(M, N, K, cus):

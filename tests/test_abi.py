@@ -31,7 +31,7 @@ def header_functions():
 
 def test_exports_every_declared_symbol():
     names = header_functions()
-    assert len(names) == 35, names
+    assert len(names) == 36, names
     lib = ctypes.CDLL(jq.LIB_PATH)
     for n in names:
         assert hasattr(lib, n), f"libjq.so does not export {n}"
@@ -302,6 +302,28 @@ def test_group_f6_validation():
     assert L.jq_w4a4g_f6_gemm_f32(A, A, 8, 128, 64, A, A, 8, MIS, None) == jq.JQ_ERR_MISALIGNED
     # operands of 2 GiB or more are refused (31-bit buffer descriptors)
     assert L.jq_w4a4g_f6_gemm_f32(A, A, 1 << 22, 65536, 64, A, A, 8, A, None) == jq.JQ_ERR_UNSUPPORTED_SHAPE
+
+
+def test_gemm_plan():
+    """The int8 GEMM's tile height: 112 rows where 128-row tiles would leave
+    the last round of blocks mostly empty and 112-row tiles fill it, else 128."""
+    plan = lambda M, N, K: jq.jq_gemm_plan(M, N, K, 256)
+    assert plan(9216, 3072, 12288) == 112   # FLUX MLP-down: 864 tiles -> 996 (two full rounds of 512)
+    assert plan(4608, 3072, 12288) == 112   # FLUX MLP-down, one image: 432 -> 504 of 512 slots
+    assert plan(4608, 12288, 3072) == 128   # FLUX MLP-up: the last 128-row round is three-eighths full
+    assert plan(4608, 3072, 3072) == 112    # DiT attention projection
+    assert plan(4608, 9216, 3072) == 112    # DiT fused QKV
+    assert plan(4096, 12288, 4096) == 128   # dLLM gate/up: whole rounds
+    assert plan(4096, 4096, 12288) == 128   # dLLM down
+    assert plan(4096, 4096, 4096) == 128    # dLLM o-proj
+    assert plan(8192, 4096, 12288) == 128   # whole rounds
+    assert plan(64, 256, 256) in (112, 128)
+    L = jq.lib()
+    t = ctypes.c_int()
+    assert L.jq_gemm_plan(8, 8, 64, 0, ctypes.byref(t)) == jq.JQ_ERR_INVALID_ARG
+    assert L.jq_gemm_plan(8, 8, 64, 256, None) == jq.JQ_ERR_INVALID_ARG
+    assert L.jq_gemm_plan(0, 8, 64, 256, ctypes.byref(t)) == jq.JQ_ERR_INVALID_ARG
+    assert L.jq_gemm_plan(8, 8, 96, 256, ctypes.byref(t)) == jq.JQ_ERR_UNSUPPORTED_SHAPE
 
 
 def test_f6_gemm_plan():
