@@ -326,6 +326,20 @@ def test_gemm_plan():
     assert L.jq_gemm_plan(8, 8, 96, 256, ctypes.byref(t)) == jq.JQ_ERR_UNSUPPORTED_SHAPE
 
 
+def test_gpu_parity_shapes_cover_both_int8_tile_heights():
+    """The GPU parity cases run the int8 GEMM at both tile heights, with M
+    ragged against each (the height is chosen per shape by the library)."""
+    from tests.test_gpu_parity import MANY_TILES, RAGGED_LINEARS
+
+    plan = lambda M, N, K: jq.jq_gemm_plan(M, N, K, 256)
+    gemm = {plan(M, N, K) for M, N, K in MANY_TILES}
+    layer = {plan(M, N, K) for M, K, N, _ in RAGGED_LINEARS}
+    assert gemm == {112, 128} and layer == {112, 128}
+    for rows in (112, 128):
+        assert any(plan(M, N, K) == rows and M % rows for M, N, K in MANY_TILES), rows
+        assert any(plan(M, N, K) == rows and M % rows for M, K, N, _ in RAGGED_LINEARS), rows
+
+
 def test_f6_gemm_plan():
     """The BF6 GEMM's block shape: one 8-wave block per CU where 256-row tiles
     cover M evenly or K is long, two 4-wave blocks (128-row tiles) otherwise."""

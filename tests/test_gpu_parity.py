@@ -220,9 +220,12 @@ def test_gemm_i32_random_codes(M, N, K):
 
 
 # Many tiles (more than one round of blocks), ragged M and N, short and
-# medium K.
-@pytest.mark.parametrize("M,N,K", [(4096, 8192, 384), (2100, 9000, 512), (300, 70000, 512), (2049, 3, 384),
-                                   (4608, 4096, 1152), (9216, 3072, 640), (33, 4099, 1536)])
+# medium K; both tile heights of the int8 GEMM (a CPU test checks that).
+MANY_TILES = [(4096, 8192, 384), (2100, 9000, 512), (300, 70000, 512), (2049, 3, 384),
+              (4608, 4096, 1152), (9216, 3072, 640), (33, 4099, 1536), (4090, 8192, 384)]
+
+
+@pytest.mark.parametrize("M,N,K", MANY_TILES)
 def test_gemm_i32_many_tiles(M, N, K):
     say("gemm i32 many tiles", M, N, K)
     qx = rand_packed(M, K, seed=M * 5 + K)
@@ -271,10 +274,12 @@ def test_linear_tiny_workload_full(with_bias):
     assert_bf16_close(y, ref, f"tiny bias={with_bias}")
 
 
-@pytest.mark.parametrize("M,K,N,bias", [(77, 3072, 130, True), (1, 64, 1, False), (5, 192, 4096, True),
-                                        (300, 1088, 260, False), (513, 256, 777, True),
-                                        (513, 1024, 777, True), (300, 6912, 777, True), (2048, 6912, 520, False),
-                                        (4100, 384, 2050, True)])
+RAGGED_LINEARS = [(77, 3072, 130, True), (1, 64, 1, False), (5, 192, 4096, True), (300, 1088, 260, False),
+                  (513, 256, 777, True), (513, 1024, 777, True), (300, 6912, 777, True), (2048, 6912, 520, False),
+                  (4100, 384, 2050, True), (4090, 384, 12288, True)]
+
+
+@pytest.mark.parametrize("M,K,N,bias", RAGGED_LINEARS)
 def test_linear_ragged(M, K, N, bias):
     say("linear ragged", M, K, N, bias)
     x = workloads.activations(M, K, "student_t3", M + 3, 0.01, 50.0)
