@@ -885,11 +885,15 @@ def main():
         "engines": {
             "bf6": {"us_per_step": head["us_per_step"], "effective_TOPS": value,
                     "pct_int8_peak": 100.0 * value / PEAK_INT8_TOPS, "per_step_us": head["per_step_us"],
-                    "warmup_steps": head["warmup_steps"]},
+                    "warmup_steps": head["warmup_steps"],
+                    "gemm_plan": {l.name: dict(zip(("waves", "tile_rows"), jq.jq_f6_gemm_plan(
+                        l.M, l.N, l.K, props.multi_processor_count))) for l in wl.linears}},
             "int8": {"us_per_step": us_int8, "effective_TOPS": wl.ops / (us_int8 * 1e-6) / 1e12,
                      "pct_int8_peak": 100.0 * wl.ops / (us_int8 * 1e-6) / 1e12 / PEAK_INT8_TOPS,
                      "per_step_us": r8["per_step_us"], "warmup_steps": r8["warmup_steps"],
                      "clock": r8.get("clock"),
+                     "gemm_plan": {l.name: {"tile_rows": jq.jq_gemm_plan(l.M, l.N, l.K, props.multi_processor_count)}
+                                   for l in wl.linears},
                      "dtype": "int8 (widened int4 codes), int32 accumulation"},
             "outputs_bit_identical": bool(engines_equal),
         },
